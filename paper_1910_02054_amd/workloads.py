@@ -1,0 +1,152 @@
+"""Seeded synthetic shard workloads.
+
+This module only describes workloads and draws their random inputs.  It holds
+none of the step's arithmetic: no layout, no statistics, no update.  Both the
+GPU path's tests/benchmark and the CPU oracle consume the very bytes it
+produces, so parity never depends on the generator.
+
+Each workload is one data-parallel rank's shard of a model shaped like those
+trained in ZeRO (arXiv 1910.02054), Sec. 10 and its appendix tables: GPT-2
+1.5B, the 13B data-parallel-only point, the 100B model at 16-way model
+parallelism x 25-way data parallelism, and a 1T model at MP 16 x N_d 1024.
+The model-parallel slice Psi/N_m is what the ZeRO-DP layout partitions.
+
+Inputs, all seeded from numpy PCG64 streams keyed by
+(seed, workload id, tensor id, step):
+
+* master parameters ~ N(0, 0.02) in fp32 (the second argument of N is a
+  standard deviation);
+* momentum and variance: zero (cold start) or N(0, 1e-4) and |N(0, 1e-6)|
+  (warm start);
+* per step, fp16 gradients = binary16(N(0, sigma) * loss_scale), with the loss
+  scale current at that step;
+* for the overflow-stress workload, at chosen 1-based steps, a fraction of
+  the gradient positions (drawn without replacement) is set to +inf or NaN
+  with probability 1/2 each;
+* the fp16 parameter output buffer starts as a sentinel pattern so that an
+  untouched buffer is detectable.
+"""
+from dataclasses import dataclass, field
+from typing import Tuple
+
+import numpy as np
+
+F16_POS_INF = 0x7C00
+F16_QNAN = 0x7E00
+P16_SENTINEL = 0x5A5A  # binary16 pattern not produced by N(0, 0.02) parameters
+
+_TENSOR_IDS = {"master": 1, "m": 2, "v": 3, "grad": 4, "inject": 5, "inject_kind": 6}
+
+
+@dataclass(frozen=True)
+class ShardWorkload:
+    key: str
+    wid: int               # workload id, part of every seed
+    description: str
+    psi: int               # elements partitioned by ZeRO-DP (the MP slice)
+    nd: int                # data-parallel degree
+    rank: int              # rank whose shard is run
+    steps: int
+    loss_scale: float      # starting loss scale
+    grad_std: float
+    warm_start: bool       # m, v drawn (True) or zero (False)
+    lr: float = 1e-4
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+    weight_decay: float = 0.0
+    clip: float = 1.0
+    master_std: float = 0.02
+    m_std: float = 1e-4
+    v_std: float = 1e-6
+    inject_steps: Tuple[int, ...] = field(default_factory=tuple)  # 1-based steps
+    inject_frac: float = 0.0
+    seed: int = 0
+
+    def hyper(self):
+        return dict(lr=self.lr, beta1=self.beta1, beta2=self.beta2, eps=self.eps,
+                    weight_decay=self.weight_decay, clip=self.clip)
+
+
+WORKLOADS = {
+    w.key: w for w in (
+        ShardWorkload("tiny", 0, "tiny shard: Psi=4,194,304 over N_d=4, rank 1",
+                      psi=4_194_304, nd=4, rank=1, steps=3, loss_scale=2.0 ** 16, grad_std=1e-3,
+                      warm_start=False),
+        ShardWorkload("gpt2_1p5b", 1, "GPT-2 1.5B over N_d=16, rank 0",
+                      psi=1_500_000_000, nd=16, rank=0, steps=10, loss_scale=2.0 ** 16, grad_std=1e-3,
+                      warm_start=True),
+        ShardWorkload("dp_13b", 2, "13B pure data parallel over N_d=64, rank 0",
+                      psi=13_000_000_000, nd=64, rank=0, steps=10, loss_scale=2.0 ** 15, grad_std=1e-2,
+                      warm_start=True),
+        ShardWorkload("mp16_dp25_100b", 3, "100B at MP 16 x N_d 25: 6.25B slice, rank 0",
+                      psi=6_250_000_000, nd=25, rank=0, steps=10, loss_scale=2.0 ** 16, grad_std=1e-3,
+                      warm_start=True),
+        ShardWorkload("ragged_1t", 4, "1T at MP 16 x N_d 1024: 62.5B slice, last rank (padded), "
+                      "inf/NaN injected at steps 3 and 7",
+                      psi=62_500_000_000, nd=1024, rank=1023, steps=12, loss_scale=2.0 ** 16, grad_std=1e-3,
+                      warm_start=True, inject_steps=(3, 7), inject_frac=1e-5),
+    )
+}
+
+
+def _rng(w: ShardWorkload, tensor: str, step: int = 0) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+        [w.seed, w.wid, _TENSOR_IDS[tensor], step])))
+
+
+def initial_state(w: ShardWorkload, n: int):
+    """(master fp32, m fp32, v fp32) for an n-element shard."""
+    master = _rng(w, "master").standard_normal(n, dtype=np.float32)
+    master *= np.float32(w.master_std)
+    if w.warm_start:
+        m = _rng(w, "m").standard_normal(n, dtype=np.float32)
+        m *= np.float32(w.m_std)
+        v = _rng(w, "v").standard_normal(n, dtype=np.float32)
+        np.abs(v, out=v)
+        v *= np.float32(w.v_std)
+    else:
+        m = np.zeros(n, np.float32)
+        v = np.zeros(n, np.float32)
+    return master, m, v
+
+
+def gradients(w: ShardWorkload, n: int, step: int, loss_scale: float) -> np.ndarray:
+    """Loss-scaled fp16 gradients for 1-based `step`, as uint16 bit patterns."""
+    z = _rng(w, "grad", step).standard_normal(n, dtype=np.float32)
+    z *= np.float32(w.grad_std * loss_scale)
+    g16 = z.astype(np.float16).view(np.uint16)
+    if step in w.inject_steps and n > 0:
+        k = max(1, int(round(w.inject_frac * n)))
+        pos = _rng(w, "inject", step).choice(n, size=min(k, n), replace=False)
+        kind = _rng(w, "inject_kind", step).integers(0, 2, size=pos.size)
+        g16[pos] = np.where(kind == 0, F16_POS_INF, F16_QNAN).astype(np.uint16)
+    return g16
+
+
+def injected_positions(w: ShardWorkload, n: int, step: int) -> np.ndarray:
+    """Positions that `gradients` overwrites with inf/NaN at `step` (empty if none)."""
+    if step not in w.inject_steps or n <= 0:
+        return np.empty(0, np.int64)
+    k = max(1, int(round(w.inject_frac * n)))
+    return np.sort(_rng(w, "inject", step).choice(n, size=min(k, n), replace=False))
+
+
+def p16_sentinel(n: int) -> np.ndarray:
+    return np.full(n, P16_SENTINEL, np.uint16)
+
+
+def random_case(seed: int, n: int, grad_std: float = 1e-3, loss_scale: float = 2.0 ** 16,
+                warm: bool = True):
+    """A free-form seeded case (g16, master, m, v) for edge-case tests."""
+    r = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 99, n])))
+    master = (r.standard_normal(n, dtype=np.float32) * np.float32(0.02)).astype(np.float32)
+    if warm:
+        m = (r.standard_normal(n, dtype=np.float32) * np.float32(1e-4)).astype(np.float32)
+        v = (np.abs(r.standard_normal(n, dtype=np.float32)) * np.float32(1e-6)).astype(np.float32)
+    else:
+        m = np.zeros(n, np.float32)
+        v = np.zeros(n, np.float32)
+    z = r.standard_normal(n, dtype=np.float32) * np.float32(grad_std * loss_scale)
+    g16 = z.astype(np.float16).view(np.uint16).copy()
+    return g16, master, m, v
