@@ -1,0 +1,197 @@
+"""Benchmark of the ZeRO P_os+g shard step on one MI355X.
+
+One step = the whole per-rank hot path over one rank's shard: the statistics
+kernels (overflow test, sum of squares, clip coefficient), the skip-flag
+readback and the fused Adam update that writes the fp16 parameter slice.
+Inputs are seeded synthetic shards resident in HBM before timing starts.
+
+Prints ONE JSON line: shard params updated per second (whole job), the step's
+HBM rate at 30 algorithmic bytes per parameter, the roofline of the dominant
+kernel (the fused update, 28 bytes per parameter, timed with HIP events on its
+own stream inside the timed region), and the CPU oracle timed on a bounded
+sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload KEY] [--no-cpu-baseline]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "shard params updated/sec and achieved HBM GB/s (% of MI355X peak)"
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
+STEP_BYTES_PER_PARAM = 30       # grad16 read twice (2+2), master/m/v read+write (24), p16 write (2)
+UPDATE_BYTES_PER_PARAM = 28     # the fused update kernel alone
+DEFAULT_WORKLOAD = "mp16_dp25_100b"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_adam_vec_mp16_dp25_100b_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1910_02054_amd", "csrc", f) for f in ("shard_kernels.hpp", "zero_shard.hip")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(n):
+    """HBM bytes per update launch from the committed counter summary, or None when
+    absent, for another shard size, or taken on a different kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    try:
+        if kv.get("kernel_source_sha256_16") != kernel_source_hash() or int(kv["shard_numel"]) != n:
+            return None
+        return float(kv["update_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
+    """The oracle, as it stands, single-threaded on a bounded prefix of the shard."""
+    import numpy as np
+    import oracle
+    chunk = 1 << 22
+    done, t_used = 0, 0.0
+    p16 = np.empty(min(n, chunk), np.uint16)
+    while done < n and t_used < budget_s:
+        b = min(n, done + chunk)
+        th, mm, vv = theta[done:b].copy(), m[done:b].copy(), v[done:b].copy()
+        t0 = time.perf_counter()
+        oracle.shard_step(g16[done:b], th, mm, vv, p16[:b - done], w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
+                          1, scale, w.clip)
+        t_used += time.perf_counter() - t0
+        done = b
+    return {"value": done / t_used, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "first %d of %d shard elements, one step (stats + update), single thread, %.1f s"
+                      % (done, n, t_used)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle CPU time")
+    ap.add_argument("--probe-copy-mib", type=int, default=0,
+                    help="also run the library's copy kernel over this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs one data-parallel rank on one GPU; --gpus %d is not supported "
+              "(the shard step needs no collective on one rank)" % max(args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1910_02054_amd import binding as zb
+    from paper_1910_02054_amd import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    w = workloads.WORKLOADS[args.workload]
+    lay = zb.zero_partition_layout(w.psi, w.nd, w.rank)
+    n = lay.valid_numel
+    print("[bench] workload %s n=%d generating inputs" % (w.key, n), file=sys.stderr, flush=True)
+    theta, m, v = workloads.initial_state(w, n)
+    g16 = workloads.gradients(w, n, 1, w.loss_scale)
+
+    def dev_f32(a):
+        return torch.from_numpy(a).to(dev)
+
+    d_theta, d_m, d_v = dev_f32(theta), dev_f32(m), dev_f32(v)
+    d_g = torch.from_numpy(g16.view(np.int16)).to(dev).view(torch.float16)
+    d_p = torch.empty(n, dtype=torch.float16, device=dev)
+    stream = torch.cuda.current_stream()
+    scaler = zb.Scaler(w.loss_scale)
+
+    def step():
+        flag = zb.zero_shard_step(d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
+                                  scaler.t_next, scaler.scale, w.clip, stream=stream)
+        scaler.update(flag)
+        return flag
+
+    if args.probe_copy_mib:
+        nb = args.probe_copy_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(7)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            zb.zero_probe_copy(src, dst, nb, stream=stream)
+        torch.cuda.synchronize()
+        del src, dst
+
+    print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    zb.zero_profile_read()
+    zb.zero_profile_enable(True)
+    skips = 0
+    print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        skips += step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    zb.zero_profile_enable(False)
+    prof = zb.zero_profile_read()
+    if skips:
+        print("bench.py: %d timed steps skipped on overflow; the measurement is invalid" % skips, file=sys.stderr)
+        sys.exit(1)
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    params_per_s = n / (ms * 1e-3)
+    step_gbps = STEP_BYTES_PER_PARAM * n / (ms * 1e-3) / 1e9
+    upd_ms = prof.update_ms / prof.steps
+    stats_ms = prof.stats_ms / prof.steps
+    upd_gbps = UPDATE_BYTES_PER_PARAM * n / (upd_ms * 1e-3) / 1e9
+    traffic = measured_traffic(n)
+
+    out = {
+        "metric": METRIC,
+        "value": params_per_s,
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.key, "description": w.description, "psi": w.psi, "nd": w.nd, "rank": w.rank,
+                   "shard_numel": n, "parallelism": "one ZeRO P_os+g data-parallel rank (N_d=%d) per GPU" % w.nd},
+        "hbm_gbps": step_gbps,
+        "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
+        "kernel_ms": {"stats_and_finalize": stats_ms, "update": upd_ms},
+        "roofline": {"bound": "hbm", "kernel": "k_adam_vec", "achieved": upd_gbps, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, n, theta, m, v, g16, w.loss_scale, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,192 @@
+/*
+ * zero_shard.h -- C ABI of libzeroshard: the per-rank optimizer step that ZeRO's
+ * P_os+g partitioning leaves on every data-parallel rank, for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Paper: ZeRO: Memory Optimizations Toward Training Trillion Parameter Models
+ * (Rajbhandari et al., arXiv 1910.02054).  Sec. 5.1: the optimizer state is
+ * split into N_d equal partitions and rank i updates only partition i, then
+ * the updated parameters are all-gathered.  Sec. 5.2: the gradients are
+ * reduce-scattered so that each rank holds only its partition's reduced
+ * gradients.  Sec. 3.1: mixed-precision Adam keeps fp16 parameters and
+ * gradients and fp32 master parameters, momentum and variance.
+ *
+ * Conventions shared by every entry point:
+ *   - Plain C types only; no exception crosses the ABI.
+ *   - Return value 0 = success (for zero_shard_step: 0 = applied, 1 = skipped),
+ *     negative = error (ZERO_E*); zero_last_error() then describes it.
+ *   - Array arguments are DEVICE pointers owned by the caller.  The library
+ *     never allocates, frees or retains them and touches exactly [0, n).
+ *   - The library owns a small per-(device, stream) workspace (per-workgroup
+ *     partial sums, one result record, one pinned host record), allocated on
+ *     first use and held until the process ends.  Its size does not depend on
+ *     n (constant-size buffers, Sec. 6.2).
+ *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.  The
+ *     device is the current HIP device of the calling thread.
+ *   - Concurrent calls are serialised per (device, stream) by the library.
+ */
+#ifndef ZERO_SHARD_H
+#define ZERO_SHARD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ZERO_OK 0
+#define ZERO_SKIPPED 1
+#define ZERO_EINVAL (-1) /* invalid argument: nothing was launched or written    */
+#define ZERO_EHIP (-2)   /* a HIP runtime call failed                             */
+#define ZERO_ENOMEM (-3) /* the library's own workspace could not be allocated    */
+
+/* ------------------------------------------------------------------------ */
+/* Partition layout                                                         */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int64_t shard_numel;  /* S = ceil(total / nd): every rank's shard length      */
+    int64_t offset;       /* rank * S: first flat index of the shard              */
+    int64_t valid_numel;  /* clamp(total - rank*S, 0, S): elements holding state */
+    int64_t padded_total; /* nd * S: length of the padded flat buffer             */
+} zero_layout_t;
+
+/* Sec. 5.1 (N_d equal partitions, rank i owns partition i).  The paper does not
+ * say what happens when nd does not divide total_numel; here the flat index
+ * space is padded at its tail, so the last rank(s) are short and a rank may
+ * hold no valid elements.  Host-only integer arithmetic, exact in int64.
+ * total_numel in [0, 2^62], nd >= 1, 0 <= rank < nd, out != NULL, else
+ * ZERO_EINVAL (out untouched). */
+int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_layout_t* out);
+
+/* ------------------------------------------------------------------------ */
+/* The shard step                                                           */
+/* ------------------------------------------------------------------------ */
+
+/* One mixed-precision Adam step over one rank's shard (Sec. 3.1, Sec. 5.1-5.2;
+ * Adam with bias correction as in Kingma & Ba, which Sec. 3.1 cites):
+ *
+ *   grad16       [n] binary16 gradients as the reduce-scatter delivers them:
+ *                averaged over ranks and still multiplied by loss_scale.
+ *                Read only.  Alignment: 2 bytes.
+ *   master32     [n] fp32 master parameters, updated in place.  4-byte aligned.
+ *   m32, v32     [n] fp32 first and second moments, updated in place.
+ *   param16_out  [n] binary16 copy of the updated master parameters (rounded
+ *                to nearest even): the slice the all-gather publishes.  Write
+ *                only.  Alignment: 2 bytes.
+ *   n            elements of the shard that hold state (the layout's
+ *                valid_numel); n == 0 returns 0 and touches nothing.
+ *   lr, beta1, beta2, eps, weight_decay
+ *                Adam hyper-parameters; beta1, beta2 in [0, 1); lr, eps >= 0
+ *                and weight_decay finite.  weight_decay != 0 adds decoupled
+ *                decay (AdamW): u += weight_decay * master before the update.
+ *   step         t >= 1: number of applied updates INCLUDING this one (bias
+ *                correction 1 - beta^t).  Skipped steps must not advance it.
+ *   loss_scale   > 0 and finite; the gradient is divided by it.
+ *   clip         global-norm clipping threshold of the unscaled gradient; the
+ *                shard's own norm is the global norm (one rank).  <= 0 disables.
+ *   stream       hipStream_t (void*), NULL = null stream.
+ *
+ * The step: overflow = any grad16 element is inf or NaN; norm =
+ * sqrt(sum grad16^2) / loss_scale; coef = clip/norm if clip > 0 and norm >
+ * clip, else 1; every element uses g = (float)grad16 * (float)(coef /
+ * loss_scale) and, in fp32,
+ *   m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g*g;
+ *   u = (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)  [+ wd*master];
+ *   master -= lr*u;  param16_out = binary16(master).
+ * On overflow nothing is written and the call returns ZERO_SKIPPED (1); the
+ * caller then lowers its loss scale and does not advance t.
+ *
+ * All five arrays must be distinct, non-overlapping ranges; base pointers of
+ * any element alignment are accepted (16-byte-aligned shards take the
+ * vectorised path).  The call blocks until the skip decision is known (a few
+ * bytes copied to pinned host memory); the update kernel may still be running
+ * on `stream` when it returns.  Returns 0 applied, 1 skipped, ZERO_EINVAL /
+ * ZERO_EHIP / ZERO_ENOMEM on error (on ZERO_EINVAL nothing is launched). */
+int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                    int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
+                    int64_t step, double loss_scale, double clip, void* stream);
+
+/* Statistics of the calling thread's last successful zero_shard_step. */
+typedef struct {
+    double sumsq;     /* sum of grad16^2 (loss-scaled), accumulated in fp64;
+                         non-finite iff overflow                                  */
+    double norm;      /* sqrt(sumsq) / loss_scale                                 */
+    double coef;      /* clipping coefficient in (0, 1]; 1 when skipped           */
+    float mult;       /* fp32 multiplier applied to grad16: (float)(coef/scale)   */
+    int32_t overflow; /* 1 if any grad16 element was inf or NaN                   */
+    int32_t skipped;  /* equals overflow                                          */
+    int32_t pad_;
+    int64_t n;        /* elements of that call                                    */
+} zero_step_stats_t;
+
+/* Copies the last step's statistics; ZERO_EINVAL if out is NULL or this
+ * thread has made no successful zero_shard_step call yet. */
+int zero_shard_last_stats(zero_step_stats_t* out);
+
+/* ------------------------------------------------------------------------ */
+/* Dynamic loss scaling (host state owned by the caller)                     */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    double scale;      /* current loss scale                                  */
+    double min_scale;  /* floor after repeated overflow                       */
+    int64_t window;    /* applied steps between doublings (<= 0: never grow)  */
+    int64_t applied;   /* updates applied so far; the next step uses t = applied + 1 */
+    int64_t good;      /* applied steps since the last overflow or growth     */
+} zero_scaler_t;
+
+/* Mixed-precision loss scaling as cited by Sec. 3.1: after a skipped step the
+ * scale halves (not below min_scale) and applied/good do not advance (good
+ * restarts); after an applied step applied and good advance and the scale
+ * doubles once good reaches window.  scale > 0 finite, min_scale > 0. */
+int zero_scaler_init(zero_scaler_t* s, double scale, int64_t window, double min_scale);
+int zero_scaler_update(zero_scaler_t* s, int32_t skipped);
+
+/* ------------------------------------------------------------------------ */
+/* Model-state memory per device (Sec. 3.1, Sec. 5.1-5.3, Table 1)           */
+/* ------------------------------------------------------------------------ */
+
+#define ZERO_STAGE_DP 0       /* (2 + 2 + K) * Psi               */
+#define ZERO_STAGE_OS 1       /* 2*Psi + 2*Psi + K*Psi/N_d       */
+#define ZERO_STAGE_OS_G 2     /* 2*Psi + (2 + K)*Psi/N_d         */
+#define ZERO_STAGE_OS_G_P 3   /* (2 + 2 + K)*Psi/N_d             */
+
+/* Bytes of model state per device for psi parameters at data-parallel degree
+ * nd (> 0) and optimizer-state multiplier k (12 for mixed-precision Adam).
+ * ZERO_EINVAL for an unknown stage, nd <= 0, psi < 0 or out == NULL. */
+int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, double* out);
+
+/* ------------------------------------------------------------------------ */
+/* Diagnostics                                                              */
+/* ------------------------------------------------------------------------ */
+
+/* Message of the calling thread's last error ("" if none).  Valid until the
+ * thread's next call into the library. */
+const char* zero_last_error(void);
+
+/* Kernel timing with HIP events on the call's own stream.  While enabled,
+ * every zero_shard_step records events around its statistics kernels and its
+ * update kernel.  zero_profile_read waits for the recorded work, then returns
+ * the summed durations and the number of steps since enabling (or the last
+ * read) and resets them. */
+typedef struct {
+    int64_t steps;      /* steps timed                                        */
+    double stats_ms;    /* total time of the statistics + finalize kernels    */
+    double update_ms;   /* total time of the fused update kernel              */
+} zero_profile_t;
+
+int zero_profile_enable(int32_t on);
+int zero_profile_read(zero_profile_t* out);
+
+/* Device-to-device copy of `bytes` bytes with the library's own streaming
+ * kernel (16-byte vectors): the achievable-bandwidth reference for the update
+ * kernel and the calibration kernel for hardware byte counters.  src and dst
+ * must be 16-byte aligned, bytes a multiple of 16, ranges disjoint. */
+int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZERO_SHARD_H */

@@ -1,0 +1,180 @@
+"""Thin ctypes binding of ``libzeroshard.so`` (C ABI in ``include/zero_shard.h``).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch supplies device memory (``data_ptr()``) and streams.  There
+is no fallback: if the library is not built, importing this module raises.
+"""
+import ctypes
+import os
+
+from . import build as _build
+
+ZERO_OK, ZERO_SKIPPED, ZERO_EINVAL, ZERO_EHIP, ZERO_ENOMEM = 0, 1, -1, -2, -3
+ZERO_STAGE_DP, ZERO_STAGE_OS, ZERO_STAGE_OS_G, ZERO_STAGE_OS_G_P = 0, 1, 2, 3
+
+if not os.path.exists(_build.LIB):
+    raise ImportError("libzeroshard.so is not built (%s); run __graft_entry__.build() or "
+                      "python paper_1910_02054_amd/build.py" % _build.LIB)
+_lib = ctypes.CDLL(_build.LIB)
+LIB_PATH = _build.LIB
+
+
+class ZeroError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s (code %d)" % (msg, code))
+        self.code = code
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("shard_numel", ctypes.c_int64), ("offset", ctypes.c_int64), ("valid_numel", ctypes.c_int64),
+                ("padded_total", ctypes.c_int64)]
+
+
+class StepStats(ctypes.Structure):
+    _fields_ = [("sumsq", ctypes.c_double), ("norm", ctypes.c_double), ("coef", ctypes.c_double),
+                ("mult", ctypes.c_float), ("overflow", ctypes.c_int32), ("skipped", ctypes.c_int32),
+                ("pad_", ctypes.c_int32), ("n", ctypes.c_int64)]
+
+
+class ScalerState(ctypes.Structure):
+    _fields_ = [("scale", ctypes.c_double), ("min_scale", ctypes.c_double), ("window", ctypes.c_int64),
+                ("applied", ctypes.c_int64), ("good", ctypes.c_int64)]
+
+
+class Profile(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("update_ms", ctypes.c_double)]
+
+
+_P, _i64, _i32, _dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+_lib.zero_partition_layout.argtypes = [_i64, _i32, _i32, ctypes.POINTER(Layout)]
+_lib.zero_shard_step.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
+_lib.zero_shard_last_stats.argtypes = [ctypes.POINTER(StepStats)]
+_lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
+_lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
+_lib.zero_model_state_bytes.argtypes = [_dbl, _dbl, _i32, _dbl, ctypes.POINTER(_dbl)]
+_lib.zero_last_error.argtypes = []
+_lib.zero_last_error.restype = ctypes.c_char_p
+_lib.zero_profile_enable.argtypes = [_i32]
+_lib.zero_profile_read.argtypes = [ctypes.POINTER(Profile)]
+_lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
+for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_last_stats", "zero_scaler_init",
+           "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
+           "zero_probe_copy"):
+    getattr(_lib, _f).restype = ctypes.c_int
+
+EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_last_stats", "zero_scaler_init",
+           "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
+           "zero_profile_read", "zero_probe_copy")
+
+
+def _check(rc):
+    if rc < 0:
+        raise ZeroError(rc, _lib.zero_last_error().decode(errors="replace"))
+    return rc
+
+
+def _addr(x, dtypes=None, what="array"):
+    """Device address of a torch tensor (checked) or a raw integer address."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if dtypes is not None and x.dtype not in dtypes:
+        raise TypeError("%s: dtype %s not in %s" % (what, x.dtype, dtypes))
+    if not x.is_cuda:
+        raise TypeError("%s must be a device tensor" % what)
+    if not x.is_contiguous():
+        raise TypeError("%s must be contiguous" % what)
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def zero_partition_layout(total_numel: int, nd: int, rank: int) -> Layout:
+    out = Layout()
+    _check(_lib.zero_partition_layout(total_numel, nd, rank, ctypes.byref(out)))
+    return out
+
+
+def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, step,
+                    loss_scale, clip, n=None, stream=None) -> int:
+    """Returns 0 (applied) or 1 (skipped on overflow); raises ZeroError on error.
+
+    Arrays are torch device tensors (grad16/param16_out float16 or int16,
+    master32/m32/v32 float32) or raw device addresses with an explicit n."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    if n is None:
+        n = grad16.numel()
+        for t in (master32, m32, v32, param16_out):
+            if t.numel() != n:
+                raise ValueError("shard tensors differ in length")
+    return _check(_lib.zero_shard_step(
+        _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(lr), float(beta1),
+        float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
+        _stream(stream)))
+
+
+def zero_shard_last_stats() -> StepStats:
+    out = StepStats()
+    _check(_lib.zero_shard_last_stats(ctypes.byref(out)))
+    return out
+
+
+class Scaler:
+    """Dynamic loss scale kept in the library's zero_scaler_t."""
+
+    def __init__(self, scale: float, window: int = 1000, min_scale: float = 1.0):
+        self.state = ScalerState()
+        _check(_lib.zero_scaler_init(ctypes.byref(self.state), scale, window, min_scale))
+
+    @property
+    def scale(self) -> float:
+        return self.state.scale
+
+    @property
+    def t_next(self) -> int:
+        return self.state.applied + 1
+
+    def update(self, skipped):
+        _check(_lib.zero_scaler_update(ctypes.byref(self.state), 1 if skipped else 0))
+
+
+def zero_model_state_bytes(psi: float, nd: float, stage: int, k: float = 12.0) -> float:
+    out = ctypes.c_double()
+    _check(_lib.zero_model_state_bytes(psi, nd, stage, k, ctypes.byref(out)))
+    return out.value
+
+
+def zero_last_error() -> str:
+    return _lib.zero_last_error().decode(errors="replace")
+
+
+def zero_profile_enable(on: bool):
+    _check(_lib.zero_profile_enable(1 if on else 0))
+
+
+def zero_profile_read() -> Profile:
+    out = Profile()
+    _check(_lib.zero_profile_read(ctypes.byref(out)))
+    return out
+
+
+def zero_probe_copy(src, dst, nbytes=None, stream=None):
+    if nbytes is None:
+        nbytes = src.numel() * src.element_size()
+    _check(_lib.zero_probe_copy(_addr(src), _addr(dst), int(nbytes), _stream(stream)))
+
+
+def raw_library():
+    """The loaded ctypes library (for ABI-level tests)."""
+    return _lib

@@ -1,0 +1,301 @@
+// shard_kernels.hpp -- gfx950 kernels of the ZeRO P_os+g shard step.
+//
+// ZeRO (arXiv 1910.02054) Sec. 5.1-5.2: after the reduce-scatter each
+// data-parallel rank holds the fp16 gradients of its 1/N_d partition and
+// updates only that partition's fp32 master parameters, momentum and variance
+// (Sec. 3.1's mixed-precision Adam), then publishes the fp16 parameters.
+//
+// Three kernels run per step, all HBM-streaming (no dense contraction, so no
+// MFMA):
+//   k_stats     one read of the fp16 gradients; per-workgroup fp64 sum of the
+//               exact fp32 squares (wave shuffle, then LDS across waves).  The
+//               sum is non-finite iff some gradient is inf or NaN, which is the
+//               overflow test (every finite square is < 2^32, so no finite
+//               sum of fewer than 2^900 of them overflows fp64).
+//   k_finalize  one workgroup: fixed-order reduction of the partial sums, the
+//               norm of the unscaled gradient, the global-norm clipping
+//               coefficient, the fp32 gradient multiplier and the skip flag.
+//   k_adam_*    the fused update: unscale+clip, Adam with bias correction,
+//               fp16 cast, 14 bytes read and 14 bytes written per element.
+//
+// Numerics: every fp32 operation of the update is correctly rounded (IEEE
+// division and square root, no contraction), in the order Adam's bias-corrected
+// form is written, so an element's result depends only on its own inputs and
+// the shared scalars.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zs {
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kStatsBlock = 256;       // threads per statistics workgroup
+constexpr int kMaxStatsBlocks = 2048;  // partial-sum records in the workspace
+constexpr int kFinalBlock = 256;
+constexpr int kAdamBlock = 256;
+
+// Per-workgroup partial of the statistics pass.
+struct alignas(16) Partial {
+    double sumsq;
+    double unused;
+};
+
+// The step's shared scalars, produced on the device by k_finalize and read by
+// the update kernel (and copied to the host for the skip decision).
+struct alignas(16) Result {
+    double sumsq;    // sum of grad16^2 (loss-scaled); non-finite iff overflow
+    double norm;     // sqrt(sumsq) / loss_scale
+    double coef;     // clipping coefficient
+    float mult;      // (float)(coef / loss_scale)
+    int32_t skip;    // 1 = overflow: the update kernel writes nothing
+    int32_t overflow;
+    int32_t unused[3];
+};
+
+// fp32 constants of the update, each rounded once from a double on the host.
+struct AdamConst {
+    float lr, b1, omb1, b2, omb2, bc1, bc2, eps, wd;
+};
+
+__device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+__device__ __forceinline__ uint32_t f32_to_f16(float x) {
+    // v_cvt_f16_f32 in the default round-to-nearest-even mode, fp16 denormals kept.
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)x);
+}
+
+// acc + g^2 for both halves of a 32-bit word; the square of a binary16 value
+// is exact in fp32 (22 significant bits) and in fp64.
+__device__ __forceinline__ double acc_sq2(uint32_t w, double acc) {
+    double lo = (double)f16_to_f32(w & 0xFFFFu);
+    double hi = (double)f16_to_f32(w >> 16);
+    acc = __builtin_fma(lo, lo, acc);
+    return __builtin_fma(hi, hi, acc);
+}
+
+__device__ __forceinline__ double sq1(uint32_t bits16) {
+    double d = (double)f16_to_f32(bits16);
+    return d * d;
+}
+
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// ---------------------------------------------------------------------------
+// K1: statistics.  `head` leading elements (0..7) are not 16-byte aligned and
+// `nvec` 8-element vectors follow; elements [head + 8*nvec, n) are the tail.
+// Grid: any number of workgroups up to kMaxStatsBlocks, kStatsBlock threads.
+// ---------------------------------------------------------------------------
+constexpr int kStatsUnroll = 4;  // 16-byte loads in flight per thread
+
+__global__ __launch_bounds__(kStatsBlock) void k_stats(const uint16_t* __restrict__ g, int64_t n, int64_t head,
+                                                       int64_t nvec, Partial* __restrict__ part) {
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    const u32x4* __restrict__ gv = reinterpret_cast<const u32x4*>(g + head);
+    const int64_t tile = (int64_t)kStatsBlock * kStatsUnroll;
+    const int64_t stride = (int64_t)gridDim.x * tile;
+    for (int64_t base = (int64_t)blockIdx.x * tile + threadIdx.x; base < nvec; base += stride) {
+        u32x4 q[kStatsUnroll];
+#pragma unroll
+        for (int u = 0; u < kStatsUnroll; ++u) {
+            const int64_t i = base + (int64_t)u * kStatsBlock;
+            q[u] = i < nvec ? __builtin_nontemporal_load(gv + i) : u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int u = 0; u < kStatsUnroll; ++u) {
+            a0 = acc_sq2(q[u].x, a0);
+            a1 = acc_sq2(q[u].y, a1);
+            a2 = acc_sq2(q[u].z, a2);
+            a3 = acc_sq2(q[u].w, a3);
+        }
+    }
+    if (blockIdx.x == 0) {
+        const int64_t t = threadIdx.x;
+        const int64_t tail0 = head + 8 * nvec;
+        if (t < head)
+            a0 += sq1(g[t]);
+        if (t < 8 && tail0 + t < n)
+            a1 += sq1(g[tail0 + t]);
+    }
+    double acc = wave_sum((a0 + a1) + (a2 + a3));
+    __shared__ double lds[kStatsBlock / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0)
+        lds[wave] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double s = 0.0;
+#pragma unroll
+        for (int w = 0; w < kStatsBlock / 64; ++w)
+            s += lds[w];
+        part[blockIdx.x].sumsq = s;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// K2: finalize.  One workgroup; fixed-order reduction, so the result depends
+// only on the partials (bitwise reproducible for a given launch shape).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restrict__ part, int nparts,
+                                                          Result* __restrict__ res, double loss_scale, double clip) {
+    double s = 0.0;
+    for (int i = threadIdx.x; i < nparts; i += kFinalBlock)
+        s += part[i].sumsq;
+    s = wave_sum(s);
+    __shared__ double lds[kFinalBlock / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0)
+        lds[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double tot = 0.0;
+#pragma unroll
+        for (int w = 0; w < kFinalBlock / 64; ++w)
+            tot += lds[w];
+        Result r;
+        r.sumsq = tot;
+        r.overflow = __builtin_isfinite(tot) ? 0 : 1;
+        r.skip = r.overflow;
+        if (r.overflow) {
+            r.norm = __builtin_inf();
+            r.coef = 1.0;
+            r.mult = 0.0f;
+        } else {
+            r.norm = __builtin_sqrt(tot) / loss_scale;
+            r.coef = (clip > 0.0 && r.norm > clip) ? clip / r.norm : 1.0;
+            r.mult = (float)(r.coef / loss_scale);
+        }
+        r.unused[0] = r.unused[1] = r.unused[2] = 0;
+        *res = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The per-element update: one definition for the vector body, the unaligned
+// head/tail and the scalar path, so every element is computed identically.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t adam_elem(uint32_t g16, float mult, float& th, float& m, float& v,
+                                              const AdamConst& c) {
+#pragma clang fp contract(off)
+    const float g = f16_to_f32(g16) * mult;
+    const float mi = c.b1 * m + c.omb1 * g;
+    const float vi = c.b2 * v + c.omb2 * (g * g);
+    const float mhat = mi / c.bc1;
+    const float vhat = vi / c.bc2;
+    const float denom = __builtin_sqrtf(vhat) + c.eps;
+    float u = mhat / denom;
+    if (c.wd != 0.0f)
+        u = u + c.wd * th;
+    th = th - c.lr * u;
+    m = mi;
+    v = vi;
+    return f32_to_f16(th);
+}
+
+__device__ __forceinline__ void adam_one(const uint16_t* g, float* th, float* m, float* v, uint16_t* p, int64_t i,
+                                         float mult, const AdamConst& c) {
+    float t = th[i], mm = m[i], vv = v[i];
+    uint32_t h = adam_elem(g[i], mult, t, mm, vv, c);
+    th[i] = t;
+    m[i] = mm;
+    v[i] = vv;
+    p[i] = (uint16_t)h;
+}
+
+// K3 (vector path).  All five arrays share the same element misalignment, so
+// after `head` (0..3) scalar elements every array is aligned for 4-element
+// vectors: 16-byte fp32 and 8-byte fp16 accesses, consecutive lanes on
+// consecutive vectors.  Each thread handles U vectors per tile, loading all of
+// them before computing.  Elements [head + 4*nvec, n) are the tail (0..3).
+template <int U>
+__global__ __launch_bounds__(kAdamBlock) void k_adam_vec(const uint16_t* __restrict__ g, float* __restrict__ th,
+                                                         float* __restrict__ m, float* __restrict__ v,
+                                                         uint16_t* __restrict__ p, int64_t n, int64_t head,
+                                                         int64_t nvec, const Result* __restrict__ res,
+                                                         AdamConst c) {
+    if (res->skip)
+        return;
+    const float mult = res->mult;
+    if (blockIdx.x == 0 && threadIdx.x < 8) {
+        const int64_t t = threadIdx.x;
+        const int64_t i = t < 4 ? t : head + 4 * nvec + (t - 4);
+        if ((t < 4 && i < head) || (t >= 4 && i < n))
+            adam_one(g, th, m, v, p, i, mult, c);
+    }
+    const u32x2* __restrict__ gv = reinterpret_cast<const u32x2*>(g + head);
+    f32x4* __restrict__ tv = reinterpret_cast<f32x4*>(th + head);
+    f32x4* __restrict__ mv = reinterpret_cast<f32x4*>(m + head);
+    f32x4* __restrict__ vv = reinterpret_cast<f32x4*>(v + head);
+    u32x2* __restrict__ pv = reinterpret_cast<u32x2*>(p + head);
+    const int64_t tile = (int64_t)kAdamBlock * U;
+    const int64_t stride = (int64_t)gridDim.x * tile;
+    for (int64_t base = (int64_t)blockIdx.x * tile + threadIdx.x; base < nvec; base += stride) {
+        u32x2 gq[U];
+        f32x4 tq[U], mq[U], vq[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kAdamBlock;
+            if (i < nvec) {
+                gq[u] = __builtin_nontemporal_load(gv + i);
+                tq[u] = __builtin_nontemporal_load(tv + i);
+                mq[u] = __builtin_nontemporal_load(mv + i);
+                vq[u] = __builtin_nontemporal_load(vv + i);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kAdamBlock;
+            if (i < nvec) {
+                float t[4] = {tq[u].x, tq[u].y, tq[u].z, tq[u].w};
+                float mm[4] = {mq[u].x, mq[u].y, mq[u].z, mq[u].w};
+                float vvv[4] = {vq[u].x, vq[u].y, vq[u].z, vq[u].w};
+                const uint32_t gw[4] = {gq[u].x & 0xFFFFu, gq[u].x >> 16, gq[u].y & 0xFFFFu, gq[u].y >> 16};
+                uint32_t h[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    h[k] = adam_elem(gw[k], mult, t[k], mm[k], vvv[k], c);
+                const f32x4 to = {t[0], t[1], t[2], t[3]};
+                const f32x4 mo = {mm[0], mm[1], mm[2], mm[3]};
+                const f32x4 vo = {vvv[0], vvv[1], vvv[2], vvv[3]};
+                const u32x2 po = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+                __builtin_nontemporal_store(to, tv + i);
+                __builtin_nontemporal_store(mo, mv + i);
+                __builtin_nontemporal_store(vo, vv + i);
+                __builtin_nontemporal_store(po, pv + i);
+            }
+        }
+    }
+}
+
+// K3 (scalar path) for arrays whose element misalignments differ.
+__global__ __launch_bounds__(kAdamBlock) void k_adam_scalar(const uint16_t* __restrict__ g, float* __restrict__ th,
+                                                            float* __restrict__ m, float* __restrict__ v,
+                                                            uint16_t* __restrict__ p, int64_t n,
+                                                            const Result* __restrict__ res, AdamConst c) {
+    if (res->skip)
+        return;
+    const float mult = res->mult;
+    const int64_t stride = (int64_t)gridDim.x * kAdamBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kAdamBlock + threadIdx.x; i < n; i += stride)
+        adam_one(g, th, m, v, p, i, mult, c);
+}
+
+// Streaming copy of nvec 16-byte vectors (bandwidth reference).
+__global__ __launch_bounds__(256) void k_probe_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                    int64_t nvec) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nvec; i += stride)
+        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+}
+
+}  // namespace zs

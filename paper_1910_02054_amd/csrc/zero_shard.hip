@@ -1,0 +1,410 @@
+// zero_shard.hip -- host side of libzeroshard: the C ABI declared in
+// include/zero_shard.h (argument checks, partition layout, fp32 constants,
+// per-(device, stream) workspace, launches, skip-flag readback, profiling).
+//
+// ZeRO (arXiv 1910.02054): Sec. 5.1 (P_os: N_d equal partitions, rank i
+// updates partition i), Sec. 5.2 (P_g: the rank holds only its partition's
+// reduced gradients), Sec. 3.1 (mixed-precision Adam state), Sec. 6.2
+// (constant-size buffers: the workspace does not grow with the shard).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "zero_shard.h"
+#include "shard_kernels.hpp"
+
+namespace {
+
+thread_local std::string t_err;
+thread_local zero_step_stats_t t_stats;
+thread_local bool t_have_stats = false;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                        \
+    do {                                                                                     \
+        hipError_t e_ = (expr);                                                              \
+        if (e_ != hipSuccess)                                                                \
+            return fail(ZERO_EHIP, "%s: %s", #expr, hipGetErrorString(e_));                  \
+    } while (0)
+
+// ---------------------------------------------------------------------------
+// Launch planning.  One function decides every launch shape from n, so tests
+// and benchmarks exercise the same configuration.
+// ---------------------------------------------------------------------------
+constexpr int kAdamUnroll = 2;
+
+struct Plan {
+    int64_t ghead, gvec;   // statistics: unaligned head elements, 8-element vectors
+    int stats_blocks;
+    bool vec;              // update: vector path (all arrays share misalignment)
+    int64_t head, nvec;    // update: head elements, 4-element vectors
+    int64_t adam_blocks;
+};
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* v, const uint16_t* p, int64_t n) {
+    Plan pl{};
+    // statistics: 16-byte vectors of the gradient
+    const uintptr_t ga = reinterpret_cast<uintptr_t>(g);
+    int64_t gh = (int64_t)(((16 - (ga & 15)) & 15) / 2);
+    pl.ghead = gh < n ? gh : n;
+    pl.gvec = (n - pl.ghead) / 8;
+    int64_t sb = ceil_div(pl.gvec, (int64_t)zs::kStatsBlock * zs::kStatsUnroll);
+    pl.stats_blocks = (int)(sb < 1 ? 1 : (sb > zs::kMaxStatsBlocks ? zs::kMaxStatsBlocks : sb));
+    // update: 4-element vectors (16-byte fp32, 8-byte fp16) need one common misalignment
+    const int64_t ef[3] = {(int64_t)((reinterpret_cast<uintptr_t>(th) & 15) / 4),
+                           (int64_t)((reinterpret_cast<uintptr_t>(m) & 15) / 4),
+                           (int64_t)((reinterpret_cast<uintptr_t>(v) & 15) / 4)};
+    const int64_t eh[2] = {(int64_t)((reinterpret_cast<uintptr_t>(g) & 7) / 2),
+                           (int64_t)((reinterpret_cast<uintptr_t>(p) & 7) / 2)};
+    pl.vec = ef[0] == ef[1] && ef[0] == ef[2] && ef[0] == eh[0] && ef[0] == eh[1];
+    if (pl.vec) {
+        int64_t h = (4 - ef[0]) & 3;
+        pl.head = h < n ? h : n;
+        pl.nvec = (n - pl.head) / 4;
+        int64_t ab = ceil_div(pl.nvec, (int64_t)zs::kAdamBlock * kAdamUnroll);
+        pl.adam_blocks = ab < 1 ? 1 : (ab > (1 << 20) ? (1 << 20) : ab);
+    } else {
+        pl.head = pl.nvec = 0;
+        int64_t ab = ceil_div(n, zs::kAdamBlock);
+        pl.adam_blocks = ab < 1 ? 1 : (ab > (1 << 20) ? (1 << 20) : ab);
+    }
+    return pl;
+}
+
+// ---------------------------------------------------------------------------
+// Per-(device, stream) context: the constant-size workspace.
+// ---------------------------------------------------------------------------
+struct Ctx {
+    std::mutex mu;
+    zs::Partial* part = nullptr;   // kMaxStatsBlocks partial records (device)
+    zs::Result* res = nullptr;     // result record (device)
+    zs::Result* host = nullptr;    // pinned host copy of the result record
+    hipEvent_t flag_ev = nullptr;  // recorded after the result copy
+};
+
+std::mutex g_ctx_mu;
+std::map<std::pair<int, hipStream_t>, std::unique_ptr<Ctx>> g_ctx;
+
+int get_ctx(hipStream_t stream, Ctx** out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lk(g_ctx_mu);
+    auto key = std::make_pair(dev, stream);
+    auto it = g_ctx.find(key);
+    if (it != g_ctx.end()) {
+        *out = it->second.get();
+        return 0;
+    }
+    std::unique_ptr<Ctx> c(new Ctx);
+    if (hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) != hipSuccess ||
+        hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) != hipSuccess ||
+        hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result), hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&c->flag_ev, hipEventDisableTiming) != hipSuccess) {
+        if (c->part) (void)hipFree(c->part);
+        if (c->res) (void)hipFree(c->res);
+        if (c->host) (void)hipHostFree(c->host);
+        if (c->flag_ev) (void)hipEventDestroy(c->flag_ev);
+        (void)hipGetLastError();
+        return fail(ZERO_ENOMEM, "could not allocate the step workspace on device %d", dev);
+    }
+    *out = c.get();
+    g_ctx.emplace(key, std::move(c));
+    return 0;
+}
+
+// ---------------------------------------------------------------------------
+// Profiling: events around the statistics and update kernels of each step.
+// ---------------------------------------------------------------------------
+struct ProfRec {
+    hipEvent_t e[4];
+};
+
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof_pending;
+std::vector<hipEvent_t> g_prof_pool;
+zero_profile_t g_prof_acc = {0, 0.0, 0.0};
+
+hipEvent_t prof_event() {
+    if (!g_prof_pool.empty()) {
+        hipEvent_t e = g_prof_pool.back();
+        g_prof_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess)
+        return nullptr;
+    return e;
+}
+
+int prof_drain_locked() {
+    for (ProfRec& r : g_prof_pending) {
+        HIP_TRY(hipEventSynchronize(r.e[3]));
+        float a = 0.f, b = 0.f;
+        HIP_TRY(hipEventElapsedTime(&a, r.e[0], r.e[1]));
+        HIP_TRY(hipEventElapsedTime(&b, r.e[2], r.e[3]));
+        g_prof_acc.steps += 1;
+        g_prof_acc.stats_ms += a;
+        g_prof_acc.update_ms += b;
+        for (hipEvent_t e : r.e)
+            g_prof_pool.push_back(e);
+    }
+    g_prof_pending.clear();
+    return 0;
+}
+
+bool is_fin(double x) { return std::isfinite(x); }
+
+bool overlaps(uintptr_t a, size_t an, uintptr_t b, size_t bn) { return a < b + bn && b < a + an; }
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+const char* zero_last_error(void) { return t_err.c_str(); }
+
+int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_layout_t* out) {
+    if (!out)
+        return fail(ZERO_EINVAL, "zero_partition_layout: out is NULL");
+    if (total_numel < 0 || total_numel > ((int64_t)1 << 62))
+        return fail(ZERO_EINVAL, "zero_partition_layout: total_numel %lld outside [0, 2^62]", (long long)total_numel);
+    if (nd < 1 || rank < 0 || rank >= nd)
+        return fail(ZERO_EINVAL, "zero_partition_layout: need nd >= 1 and 0 <= rank < nd (nd=%d rank=%d)", nd, rank);
+    const int64_t shard = total_numel / nd + (total_numel % nd ? 1 : 0);
+    const int64_t first = shard * rank;
+    int64_t valid = total_numel - first;
+    valid = valid < 0 ? 0 : (valid > shard ? shard : valid);
+    out->shard_numel = shard;
+    out->offset = first;
+    out->valid_numel = valid;
+    out->padded_total = shard * nd;
+    return ZERO_OK;
+}
+
+int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, double* out) {
+    if (!out || !(nd > 0.0) || !(psi >= 0.0) || !is_fin(k))
+        return fail(ZERO_EINVAL, "zero_model_state_bytes: invalid psi/nd/k or NULL out");
+    // fp16 parameters and gradients take 2 bytes each, the optimizer state K bytes per parameter.
+    const double params = 2.0 * psi, grads = 2.0 * psi, opt = k * psi;
+    switch (stage) {
+    case ZERO_STAGE_DP: *out = params + grads + opt; break;
+    case ZERO_STAGE_OS: *out = params + grads + opt / nd; break;
+    case ZERO_STAGE_OS_G: *out = params + (grads + opt) / nd; break;
+    case ZERO_STAGE_OS_G_P: *out = (params + grads + opt) / nd; break;
+    default: return fail(ZERO_EINVAL, "zero_model_state_bytes: unknown stage %d", stage);
+    }
+    return ZERO_OK;
+}
+
+int zero_scaler_init(zero_scaler_t* s, double scale, int64_t window, double min_scale) {
+    if (!s || !is_fin(scale) || !(scale > 0.0) || !is_fin(min_scale) || !(min_scale > 0.0))
+        return fail(ZERO_EINVAL, "zero_scaler_init: need finite scale > 0 and min_scale > 0");
+    s->scale = scale;
+    s->min_scale = min_scale;
+    s->window = window;
+    s->applied = 0;
+    s->good = 0;
+    return ZERO_OK;
+}
+
+int zero_scaler_update(zero_scaler_t* s, int32_t skipped) {
+    if (!s)
+        return fail(ZERO_EINVAL, "zero_scaler_update: NULL scaler");
+    if (skipped) {
+        const double halved = s->scale * 0.5;
+        s->scale = halved > s->min_scale ? halved : s->min_scale;
+        s->good = 0;
+    } else {
+        s->applied += 1;
+        s->good += 1;
+        if (s->window > 0 && s->good >= s->window) {
+            s->scale *= 2.0;
+            s->good = 0;
+        }
+    }
+    return ZERO_OK;
+}
+
+int zero_shard_last_stats(zero_step_stats_t* out) {
+    if (!out)
+        return fail(ZERO_EINVAL, "zero_shard_last_stats: NULL out");
+    if (!t_have_stats)
+        return fail(ZERO_EINVAL, "zero_shard_last_stats: no step on this thread yet");
+    *out = t_stats;
+    return ZERO_OK;
+}
+
+int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                    int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
+                    int64_t step, double loss_scale, double clip, void* stream_) {
+    // ---- argument checks: nothing is launched unless all pass ----
+    if (n < 0 || n > ((int64_t)1 << 40))
+        return fail(ZERO_EINVAL, "zero_shard_step: n=%lld outside [0, 2^40]", (long long)n);
+    if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
+        return fail(ZERO_EINVAL, "zero_shard_step: need finite lr >= 0, eps >= 0, weight_decay");
+    if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+        return fail(ZERO_EINVAL, "zero_shard_step: beta1, beta2 must lie in [0, 1)");
+    if (step < 1)
+        return fail(ZERO_EINVAL, "zero_shard_step: step (t) must be >= 1, got %lld", (long long)step);
+    if (!is_fin(loss_scale) || !(loss_scale > 0.0))
+        return fail(ZERO_EINVAL, "zero_shard_step: loss_scale must be finite and > 0");
+    if (std::isnan(clip))
+        return fail(ZERO_EINVAL, "zero_shard_step: clip is NaN");
+    if (n > 0) {
+        if (!grad16 || !master32 || !m32 || !v32 || !param16_out)
+            return fail(ZERO_EINVAL, "zero_shard_step: NULL array with n > 0");
+        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
+                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
+                                reinterpret_cast<uintptr_t>(param16_out)};
+        const size_t sz[5] = {2, 4, 4, 4, 2};
+        for (int i = 0; i < 5; ++i)
+            if (a[i] % sz[i])
+                return fail(ZERO_EINVAL, "zero_shard_step: array %d is not %zu-byte aligned", i, sz[i]);
+        for (int i = 0; i < 5; ++i)
+            for (int j = i + 1; j < 5; ++j)
+                if (overlaps(a[i], sz[i] * (size_t)n, a[j], sz[j] * (size_t)n))
+                    return fail(ZERO_EINVAL, "zero_shard_step: arrays %d and %d overlap", i, j);
+    }
+    if (n == 0) {
+        t_stats = zero_step_stats_t{0.0, 0.0, 1.0, (float)(1.0 / loss_scale), 0, 0, 0, 0};
+        t_have_stats = true;
+        return ZERO_OK;
+    }
+
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    int rc = get_ctx(stream, &ctx);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+
+    // fp32 constants, each computed in double and rounded once (the bias
+    // corrections 1 - beta^t use the C library's pow).
+    zs::AdamConst c;
+    c.lr = (float)lr;
+    c.b1 = (float)beta1;
+    c.omb1 = (float)(1.0 - beta1);
+    c.b2 = (float)beta2;
+    c.omb2 = (float)(1.0 - beta2);
+    c.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
+    c.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
+    c.eps = (float)eps;
+    c.wd = (float)weight_decay;
+
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n);
+
+    ProfRec pr{};
+    bool prof = false;
+    {
+        std::lock_guard<std::mutex> plk(g_prof_mu);
+        if (g_prof_on) {
+            prof = true;
+            for (hipEvent_t& e : pr.e)
+                if (!(e = prof_event()))
+                    return fail(ZERO_EHIP, "zero_shard_step: could not create a profiling event");
+        }
+    }
+
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[0], stream));
+    zs::k_stats<<<pl.stats_blocks, zs::kStatsBlock, 0, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+    HIP_TRY(hipGetLastError());
+    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, loss_scale, clip);
+    HIP_TRY(hipGetLastError());
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[1], stream));
+    HIP_TRY(hipMemcpyAsync(ctx->host, ctx->res, sizeof(zs::Result), hipMemcpyDeviceToHost, stream));
+    HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[2], stream));
+    if (pl.vec)
+        zs::k_adam_vec<kAdamUnroll><<<(unsigned)pl.adam_blocks, zs::kAdamBlock, 0, stream>>>(
+            grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
+    else
+        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kAdamBlock, 0, stream>>>(
+            grad16, master32, m32, v32, param16_out, n, ctx->res, c);
+    HIP_TRY(hipGetLastError());
+    if (prof) {
+        HIP_TRY(hipEventRecord(pr.e[3], stream));
+        std::lock_guard<std::mutex> plk(g_prof_mu);
+        g_prof_pending.push_back(pr);
+        if (g_prof_pending.size() >= 4096) {
+            int r2 = prof_drain_locked();
+            if (r2)
+                return r2;
+        }
+    }
+    // The update kernel is already queued behind the copy: wait only for the flag.
+    HIP_TRY(hipEventSynchronize(ctx->flag_ev));
+    const zs::Result r = *ctx->host;
+    t_stats.sumsq = r.sumsq;
+    t_stats.norm = r.norm;
+    t_stats.coef = r.coef;
+    t_stats.mult = r.mult;
+    t_stats.overflow = r.overflow;
+    t_stats.skipped = r.skip;
+    t_stats.pad_ = 0;
+    t_stats.n = n;
+    t_have_stats = true;
+    return r.skip ? ZERO_SKIPPED : ZERO_OK;
+}
+
+int zero_profile_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_on = on != 0;
+    return ZERO_OK;
+}
+
+int zero_profile_read(zero_profile_t* out) {
+    if (!out)
+        return fail(ZERO_EINVAL, "zero_profile_read: NULL out");
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    int rc = prof_drain_locked();
+    if (rc)
+        return rc;
+    *out = g_prof_acc;
+    g_prof_acc = zero_profile_t{0, 0.0, 0.0};
+    return ZERO_OK;
+}
+
+int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {
+    const uintptr_t s = reinterpret_cast<uintptr_t>(src), d = reinterpret_cast<uintptr_t>(dst);
+    if (bytes < 0 || bytes % 16 || (bytes > 0 && (!src || !dst || s % 16 || d % 16)))
+        return fail(ZERO_EINVAL, "zero_probe_copy: need 16-byte aligned buffers and a multiple of 16 bytes");
+    if (bytes > 0 && overlaps(s, (size_t)bytes, d, (size_t)bytes))
+        return fail(ZERO_EINVAL, "zero_probe_copy: ranges overlap");
+    if (bytes == 0)
+        return ZERO_OK;
+    const int64_t nvec = bytes / 16;
+    int64_t blocks = ceil_div(nvec, 256 * 4);
+    blocks = blocks < 1 ? 1 : (blocks > (1 << 20) ? (1 << 20) : blocks);
+    zs::k_probe_copy<<<(unsigned)blocks, 256, 0, reinterpret_cast<hipStream_t>(stream_)>>>(
+        reinterpret_cast<const zs::u32x4*>(src), reinterpret_cast<zs::u32x4*>(dst), nvec);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+}  // extern "C"

@@ -12,7 +12,8 @@ parallelism x 25-way data parallelism, and a 1T model at MP 16 x N_d 1024.
 The model-parallel slice Psi/N_m is what the ZeRO-DP layout partitions.
 
 Inputs, all seeded from numpy PCG64 streams keyed by
-(seed, workload id, tensor id, step):
+(seed, workload id, tensor id, step, chunk), one stream per 2^22-element chunk
+so that chunks can be drawn in parallel threads:
 
 * master parameters ~ N(0, 0.02) in fp32 (the second argument of N is a
   standard deviation);
@@ -26,6 +27,8 @@ Inputs, all seeded from numpy PCG64 streams keyed by
 * the fp16 parameter output buffer starts as a sentinel pattern so that an
   untouched buffer is detectable.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 from typing import Tuple
 
@@ -90,21 +93,48 @@ WORKLOADS = {
 }
 
 
-def _rng(w: ShardWorkload, tensor: str, step: int = 0) -> np.random.Generator:
+CHUNK = 1 << 22
+_POOL = None
+
+
+def _pool():
+    global _POOL
+    if _POOL is None:
+        try:
+            k = len(os.sched_getaffinity(0))
+        except AttributeError:
+            k = 4
+        _POOL = ThreadPoolExecutor(max_workers=max(1, min(16, k)))
+    return _POOL
+
+
+def _rng(w: ShardWorkload, tensor: str, step: int = 0, chunk: int = 0) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence(
-        [w.seed, w.wid, _TENSOR_IDS[tensor], step])))
+        [w.seed, w.wid, _TENSOR_IDS[tensor], step, chunk])))
+
+
+def _normal(w: ShardWorkload, tensor: str, step: int, n: int, std: float, absolute: bool = False,
+            out_dtype=np.float32) -> np.ndarray:
+    """n draws of N(0, std) (|N(0, std)| if absolute) in fp32, cast to out_dtype."""
+    out = np.empty(n, out_dtype)
+
+    def fill(c):
+        a, b = c * CHUNK, min(n, (c + 1) * CHUNK)
+        z = _rng(w, tensor, step, c).standard_normal(b - a, dtype=np.float32)
+        if absolute:
+            np.abs(z, out=z)
+        z *= np.float32(std)
+        out[a:b] = z  # fp32 -> out_dtype, round to nearest even
+    list(_pool().map(fill, range((n + CHUNK - 1) // CHUNK)))
+    return out
 
 
 def initial_state(w: ShardWorkload, n: int):
     """(master fp32, m fp32, v fp32) for an n-element shard."""
-    master = _rng(w, "master").standard_normal(n, dtype=np.float32)
-    master *= np.float32(w.master_std)
+    master = _normal(w, "master", 0, n, w.master_std)
     if w.warm_start:
-        m = _rng(w, "m").standard_normal(n, dtype=np.float32)
-        m *= np.float32(w.m_std)
-        v = _rng(w, "v").standard_normal(n, dtype=np.float32)
-        np.abs(v, out=v)
-        v *= np.float32(w.v_std)
+        m = _normal(w, "m", 0, n, w.m_std)
+        v = _normal(w, "v", 0, n, w.v_std, absolute=True)
     else:
         m = np.zeros(n, np.float32)
         v = np.zeros(n, np.float32)
@@ -113,9 +143,7 @@ def initial_state(w: ShardWorkload, n: int):
 
 def gradients(w: ShardWorkload, n: int, step: int, loss_scale: float) -> np.ndarray:
     """Loss-scaled fp16 gradients for 1-based `step`, as uint16 bit patterns."""
-    z = _rng(w, "grad", step).standard_normal(n, dtype=np.float32)
-    z *= np.float32(w.grad_std * loss_scale)
-    g16 = z.astype(np.float16).view(np.uint16)
+    g16 = _normal(w, "grad", step, n, w.grad_std * loss_scale, out_dtype=np.float16).view(np.uint16)
     if step in w.inject_steps and n > 0:
         k = max(1, int(round(w.inject_frac * n)))
         pos = _rng(w, "inject", step).choice(n, size=min(k, n), replace=False)

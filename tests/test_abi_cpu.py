@@ -1,0 +1,131 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and its host-only entry points (layout, accounting, loss scaler,
+argument validation) agree with the oracle.  No GPU work is launched here:
+every zero_shard_step call below is rejected (or is a no-op) before any HIP
+call is made."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zero_shard.h")
+
+
+@pytest.fixture(scope="module")
+def zb():
+    from paper_1910_02054_amd import build as b
+    if b.is_stale():
+        b.build()
+    from paper_1910_02054_amd import binding
+    return binding
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\**(zero_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = _declared()
+    for required in ("zero_partition_layout", "zero_shard_step", "zero_last_error"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(zb):
+    names = _declared()
+    lib = zb.raw_library()
+    for name in names:
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", zb.LIB_PATH], stdout=subprocess.PIPE, check=True).stdout.decode()
+    exported = set(re.findall(r"\bT (zero_\w+)", out))
+    assert set(names) <= exported
+    assert set(zb.EXPORTS) == set(names)
+
+
+def test_layout_bitwise_vs_oracle(zb):
+    for psi in list(range(0, 40)) + [4_194_304, 4_194_305, 1_500_000_000, 13_000_000_000, 6_250_000_000,
+                                     62_500_000_000, (1 << 62)]:
+        for nd in (1, 2, 3, 4, 7, 16, 25, 64, 1024):
+            for rank in sorted({0, 1, nd // 2, nd - 1}):
+                if rank >= nd:
+                    continue
+                lay = zb.zero_partition_layout(psi, nd, rank)
+                assert (lay.shard_numel, lay.offset, lay.valid_numel, lay.padded_total) == oracle.layout(psi, nd, rank)
+
+
+@pytest.mark.parametrize("psi,nd,rank", [(-1, 4, 0), (10, 0, 0), (10, 4, 4), (10, 4, -1), ((1 << 62) + 1, 2, 0)])
+def test_layout_rejects(zb, psi, nd, rank):
+    with pytest.raises(zb.ZeroError) as e:
+        zb.zero_partition_layout(psi, nd, rank)
+    assert e.value.code == zb.ZERO_EINVAL
+
+
+def test_model_state_bytes_vs_oracle(zb):
+    for psi in (7.5e9, 128e9, 1e12, 1.5e9, 1.0):
+        for nd in (1, 4, 16, 64, 256, 1024):
+            for stage in range(4):
+                got = zb.zero_model_state_bytes(psi, nd, stage)
+                assert got == pytest.approx(oracle.model_state_bytes(psi, nd, stage), rel=1e-15)
+    with pytest.raises(zb.ZeroError):
+        zb.zero_model_state_bytes(1e9, 4, 9)
+
+
+def test_scaler_matches_oracle(zb):
+    rng = np.random.default_rng(0)
+    for window in (0, 1, 3, 1000):
+        a = zb.Scaler(2.0 ** 16, window=window, min_scale=1.0)
+        b = oracle.Scaler(2.0 ** 16, window=window, min_scale=1.0)
+        for skipped in rng.integers(0, 2, size=60):
+            assert a.t_next == b.t_next
+            a.update(int(skipped))
+            b.update(int(skipped))
+            assert a.scale == b.scale.value and a.state.applied == b.applied.value and a.state.good == b.good.value
+
+
+def _step_raw(zb, ptrs, n, **kw):
+    args = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0, step=1, scale=65536.0, clip=1.0)
+    args.update(kw)
+    lib = zb.raw_library()
+    return lib.zero_shard_step(*ptrs, n, args["lr"], args["beta1"], args["beta2"], args["eps"], args["wd"],
+                               args["step"], args["scale"], args["clip"], None)
+
+
+# Fake, never-dereferenced addresses: validation must reject these calls before any HIP call.
+GOOD = [0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000]
+
+
+@pytest.mark.parametrize("kw,ptrs,n", [
+    (dict(), GOOD, -1),
+    (dict(), [0] + GOOD[1:], 10),
+    (dict(), [GOOD[0] + 1] + GOOD[1:], 10),             # fp16 misaligned to 1 byte
+    (dict(), GOOD[:1] + [GOOD[1] + 2] + GOOD[2:], 10),  # fp32 misaligned to 2 bytes
+    (dict(), [GOOD[0], GOOD[1], GOOD[1] + 8] + GOOD[3:], 10),  # master and m overlap
+    (dict(), [GOOD[0], GOOD[1], GOOD[2], GOOD[3], GOOD[0] + 4], 10),  # p16 overlaps grads
+    (dict(beta1=1.0), GOOD, 10),
+    (dict(beta2=-0.1), GOOD, 10),
+    (dict(step=0), GOOD, 10),
+    (dict(scale=0.0), GOOD, 10),
+    (dict(scale=float("inf")), GOOD, 10),
+    (dict(lr=float("nan")), GOOD, 10),
+    (dict(lr=-1.0), GOOD, 10),
+    (dict(eps=-1e-8), GOOD, 10),
+    (dict(clip=float("nan")), GOOD, 10),
+    (dict(wd=float("inf")), GOOD, 10),
+    (dict(), GOOD, (1 << 40) + 1),
+])
+def test_step_rejects_invalid_arguments(zb, kw, ptrs, n):
+    assert _step_raw(zb, ptrs, n, **kw) == zb.ZERO_EINVAL
+    assert zb.zero_last_error() != ""
+
+
+def test_step_with_zero_elements_is_a_noop(zb):
+    assert _step_raw(zb, [0, 0, 0, 0, 0], 0) == zb.ZERO_OK
+    st = zb.zero_shard_last_stats()
+    assert st.n == 0 and st.skipped == 0
