@@ -87,7 +87,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle CPU time")
-    ap.add_argument("--probe-copy-mib", type=int, default=0,
+    ap.add_argument("--probe-copy-mib", type=int, default=2048,
                     help="also run the library's copy kernel over this many MiB (counter calibration)")
     args = ap.parse_args()
 
@@ -111,30 +111,45 @@ def main():
     n = lay.valid_numel
     print("[bench] workload %s n=%d generating inputs" % (w.key, n), file=sys.stderr, flush=True)
     theta, m, v = workloads.initial_state(w, n)
-    g16 = workloads.gradients(w, n, 1, w.loss_scale)
+    # two gradient batches, alternated step by step as fresh reduce-scattered gradients would be
+    g16s = [workloads.gradients(w, n, k, w.loss_scale) for k in (1, 2)]
+    g16 = g16s[0]
 
     def dev_f32(a):
         return torch.from_numpy(a).to(dev)
 
     d_theta, d_m, d_v = dev_f32(theta), dev_f32(m), dev_f32(v)
-    d_g = torch.from_numpy(g16.view(np.int16)).to(dev).view(torch.float16)
+    d_gs = [torch.from_numpy(g.view(np.int16)).to(dev).view(torch.float16) for g in g16s]
     d_p = torch.empty(n, dtype=torch.float16, device=dev)
     stream = torch.cuda.current_stream()
     scaler = zb.Scaler(w.loss_scale)
 
     def step():
+        d_g = d_gs[scaler.t_next % 2]
         flag = zb.zero_shard_step(d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
                                   scaler.t_next, scaler.scale, w.clip, stream=stream)
         scaler.update(flag)
         return flag
 
+    probe = None
     if args.probe_copy_mib:
+        # achievable streaming rate on this GPU: the library's 16-byte copy kernel, timed with
+        # events on the stream it runs on (read + write bytes per launch)
         nb = args.probe_copy_mib << 20
         src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(7)
         dst = torch.empty_like(src)
         for _ in range(3):
             zb.zero_probe_copy(src, dst, nb, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 20
+        e0.record(stream)
+        for _ in range(reps):
+            zb.zero_probe_copy(src, dst, nb, stream=stream)
+        e1.record(stream)
         torch.cuda.synchronize()
+        cms = e0.elapsed_time(e1) / reps
+        probe = {"kernel": "k_probe_copy", "bytes_per_launch": 2 * nb, "ms": cms,
+                 "gbps": 2 * nb / (cms * 1e-3) / 1e9}
         del src, dst
 
     print("[bench] warmup %d" % args.warmup, file=sys.stderr, flush=True)
@@ -187,6 +202,9 @@ def main():
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
     }
+    if probe:
+        probe["update_frac_of_copy"] = upd_gbps / probe["gbps"]
+        out["copy_probe"] = probe
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, n, theta, m, v, g16, w.loss_scale, args.cpu_budget)

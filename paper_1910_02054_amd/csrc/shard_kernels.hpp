@@ -10,13 +10,14 @@
 //   k_stats     one read of the fp16 gradients; per-workgroup fp64 sum of the
 //               exact fp32 squares (wave shuffle, then LDS across waves).  The
 //               sum is non-finite iff some gradient is inf or NaN, which is the
-//               overflow test (every finite square is < 2^32, so no finite
-//               sum of fewer than 2^900 of them overflows fp64).
-//   k_finalize  one workgroup: fixed-order reduction of the partial sums, the
-//               norm of the unscaled gradient, the global-norm clipping
-//               coefficient, the fp32 gradient multiplier and the skip flag.
-//   k_adam_*    the fused update: unscale+clip, Adam with bias correction,
-//               fp16 cast, 14 bytes read and 14 bytes written per element.
+//               overflow test (every finite square is below 2^32, so no finite
+//               sum over fewer than 2^990 elements overflows fp64).
+//   k_finalize  one workgroup: fixed-order reduction of the partials; the norm
+//               of the unscaled gradient, the global-norm clipping coefficient,
+//               the fp32 gradient multiplier and the skip flag, written to
+//               device memory and to a host-mapped record.
+//   k_adam_*    the fused update: unscale+clip, Adam with bias correction, fp16
+//               cast; 14 bytes read and 14 bytes written per element.
 //
 // Numerics: every fp32 operation of the update is correctly rounded (IEEE
 // division and square root, no contraction), in the order Adam's bias-corrected
@@ -33,10 +34,40 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kStatsBlock = 256;       // threads per statistics workgroup
-constexpr int kMaxStatsBlocks = 2048;  // partial-sum records in the workspace
-constexpr int kFinalBlock = 256;
-constexpr int kAdamBlock = 256;
+constexpr int kMaxStatsBlocks = 4096;  // partial-sum records in the workspace
+constexpr int kScalarBlock = 256;
+
+// Launch-policy knobs of the streaming kernels are template parameters:
+//   BLOCK  threads per workgroup;  U  vectors per thread per tile;
+//   NTL/NTS  non-temporal (streaming) loads/stores;
+//   XCD    remap workgroups so that each of the 8 XCDs walks a contiguous run of
+//          tiles (the dispatcher assigns workgroup b to XCD b mod 8);
+//   REV    walk the tiles from the end of the shard to its start.
+template <bool NT, typename T>
+__device__ __forceinline__ T ld(const T* p) {
+    if constexpr (NT)
+        return __builtin_nontemporal_load(p);
+    else
+        return *p;
+}
+
+template <bool NT, typename T>
+__device__ __forceinline__ void st(T v, T* p) {
+    if constexpr (NT)
+        __builtin_nontemporal_store(v, p);
+    else
+        *p = v;
+}
+
+template <bool XCD>
+__device__ __forceinline__ int64_t logical_block() {
+    const unsigned b = blockIdx.x, grid = gridDim.x;
+    if constexpr (XCD) {
+        if (grid % 8 == 0)
+            return (int64_t)(b % 8) * (grid / 8) + b / 8;  // a bijection of [0, grid)
+    }
+    return b;
+}
 
 // Per-workgroup partial of the statistics pass.
 struct alignas(16) Partial {
@@ -45,7 +76,8 @@ struct alignas(16) Partial {
 };
 
 // The step's shared scalars, produced on the device by k_finalize and read by
-// the update kernel (and copied to the host for the skip decision).
+// the update kernel (and by the host through a mapped copy for the skip
+// decision).
 struct alignas(16) Result {
     double sumsq;    // sum of grad16^2 (loss-scaled); non-finite iff overflow
     double norm;     // sqrt(sumsq) / loss_scale
@@ -53,7 +85,8 @@ struct alignas(16) Result {
     float mult;      // (float)(coef / loss_scale)
     int32_t skip;    // 1 = overflow: the update kernel writes nothing
     int32_t overflow;
-    int32_t unused[3];
+    uint32_t seq;    // call sequence number, echoed so the host can check freshness
+    int32_t unused[2];
 };
 
 // fp32 constants of the update, each rounded once from a double on the host.
@@ -91,28 +124,72 @@ __device__ __forceinline__ double wave_sum(double x) {
     return x;
 }
 
+// Fixed-order sum of one double per thread over a workgroup of BLOCK threads;
+// the total is returned to thread 0.
+template <int BLOCK>
+__device__ __forceinline__ double block_sum(double x) {
+    __shared__ double lds[BLOCK / 64];
+    x = wave_sum(x);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if constexpr (BLOCK == 64) {
+        return x;
+    } else {
+        if (lane == 0)
+            lds[wave] = x;
+        __syncthreads();
+        double s = 0.0;
+        if (threadIdx.x == 0) {
+#pragma unroll
+            for (int w = 0; w < BLOCK / 64; ++w)
+                s += lds[w];
+        }
+        return s;
+    }
+}
+
+// Norm, clipping coefficient, multiplier and skip flag from the global sum of
+// squares (all in double; the multiplier rounded once to fp32).
+__device__ __forceinline__ Result make_result(double tot, double loss_scale, double clip, uint32_t seq) {
+    Result r;
+    r.sumsq = tot;
+    r.overflow = __builtin_isfinite(tot) ? 0 : 1;
+    r.skip = r.overflow;
+    if (r.overflow) {
+        r.norm = __builtin_inf();
+        r.coef = 1.0;
+        r.mult = 0.0f;
+    } else {
+        r.norm = __builtin_sqrt(tot) / loss_scale;
+        r.coef = (clip > 0.0 && r.norm > clip) ? clip / r.norm : 1.0;
+        r.mult = (float)(r.coef / loss_scale);
+    }
+    r.seq = seq;
+    r.unused[0] = r.unused[1] = 0;
+    return r;
+}
+
 // ---------------------------------------------------------------------------
 // K1: statistics.  `head` leading elements (0..7) are not 16-byte aligned and
 // `nvec` 8-element vectors follow; elements [head + 8*nvec, n) are the tail.
-// Grid: any number of workgroups up to kMaxStatsBlocks, kStatsBlock threads.
+// Grid: 1 .. kMaxStatsBlocks workgroups of BLOCK threads; workgroup b writes
+// part[b].
 // ---------------------------------------------------------------------------
-constexpr int kStatsUnroll = 4;  // 16-byte loads in flight per thread
-
-__global__ __launch_bounds__(kStatsBlock) void k_stats(const uint16_t* __restrict__ g, int64_t n, int64_t head,
-                                                       int64_t nvec, Partial* __restrict__ part) {
+template <int BLOCK, int U, bool NTL, bool XCD>
+__global__ __launch_bounds__(BLOCK) void k_stats(const uint16_t* __restrict__ g, int64_t n, int64_t head,
+                                                 int64_t nvec, Partial* __restrict__ part) {
     double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
     const u32x4* __restrict__ gv = reinterpret_cast<const u32x4*>(g + head);
-    const int64_t tile = (int64_t)kStatsBlock * kStatsUnroll;
+    const int64_t tile = (int64_t)BLOCK * U;
     const int64_t stride = (int64_t)gridDim.x * tile;
-    for (int64_t base = (int64_t)blockIdx.x * tile + threadIdx.x; base < nvec; base += stride) {
-        u32x4 q[kStatsUnroll];
+    for (int64_t base = logical_block<XCD>() * tile + threadIdx.x; base < nvec; base += stride) {
+        u32x4 q[U];
 #pragma unroll
-        for (int u = 0; u < kStatsUnroll; ++u) {
-            const int64_t i = base + (int64_t)u * kStatsBlock;
-            q[u] = i < nvec ? __builtin_nontemporal_load(gv + i) : u32x4{0u, 0u, 0u, 0u};
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * BLOCK;
+            q[u] = i < nvec ? ld<NTL>(gv + i) : u32x4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
-        for (int u = 0; u < kStatsUnroll; ++u) {
+        for (int u = 0; u < U; ++u) {
             a0 = acc_sq2(q[u].x, a0);
             a1 = acc_sq2(q[u].y, a1);
             a2 = acc_sq2(q[u].z, a2);
@@ -127,56 +204,36 @@ __global__ __launch_bounds__(kStatsBlock) void k_stats(const uint16_t* __restric
         if (t < 8 && tail0 + t < n)
             a1 += sq1(g[tail0 + t]);
     }
-    double acc = wave_sum((a0 + a1) + (a2 + a3));
-    __shared__ double lds[kStatsBlock / 64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0)
-        lds[wave] = acc;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        double s = 0.0;
-#pragma unroll
-        for (int w = 0; w < kStatsBlock / 64; ++w)
-            s += lds[w];
+    const double s = block_sum<BLOCK>((a0 + a1) + (a2 + a3));
+    if (threadIdx.x == 0)
         part[blockIdx.x].sumsq = s;
-    }
 }
 
 // ---------------------------------------------------------------------------
-// K2: finalize.  One workgroup; fixed-order reduction, so the result depends
-// only on the partials (bitwise reproducible for a given launch shape).
+// K2: finalize.  One workgroup of kFinalBlock threads; fixed-order reduction,
+// so the result depends only on the partials (bitwise reproducible for a given
+// launch shape).  `res_host` is host-mapped; the system-scope fence makes the
+// record visible to the host once the kernel has completed.
 // ---------------------------------------------------------------------------
+constexpr int kFinalBlock = 256;
+
 __global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restrict__ part, int nparts,
-                                                          Result* __restrict__ res, double loss_scale, double clip) {
-    double s = 0.0;
-    for (int i = threadIdx.x; i < nparts; i += kFinalBlock)
-        s += part[i].sumsq;
-    s = wave_sum(s);
-    __shared__ double lds[kFinalBlock / 64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0)
-        lds[wave] = s;
-    __syncthreads();
+                                                          Result* __restrict__ res, Result* __restrict__ res_host,
+                                                          double loss_scale, double clip, uint32_t seq) {
+    double s0 = 0.0, s1 = 0.0;
+    int i = threadIdx.x;
+    for (; i + kFinalBlock < nparts; i += 2 * kFinalBlock) {
+        s0 += part[i].sumsq;
+        s1 += part[i + kFinalBlock].sumsq;
+    }
+    if (i < nparts)
+        s0 += part[i].sumsq;
+    const double tot = block_sum<kFinalBlock>(s0 + s1);
     if (threadIdx.x == 0) {
-        double tot = 0.0;
-#pragma unroll
-        for (int w = 0; w < kFinalBlock / 64; ++w)
-            tot += lds[w];
-        Result r;
-        r.sumsq = tot;
-        r.overflow = __builtin_isfinite(tot) ? 0 : 1;
-        r.skip = r.overflow;
-        if (r.overflow) {
-            r.norm = __builtin_inf();
-            r.coef = 1.0;
-            r.mult = 0.0f;
-        } else {
-            r.norm = __builtin_sqrt(tot) / loss_scale;
-            r.coef = (clip > 0.0 && r.norm > clip) ? clip / r.norm : 1.0;
-            r.mult = (float)(r.coef / loss_scale);
-        }
-        r.unused[0] = r.unused[1] = r.unused[2] = 0;
+        const Result r = make_result(tot, loss_scale, clip, seq);
         *res = r;
+        *res_host = r;
+        __threadfence_system();
     }
 }
 
@@ -212,17 +269,17 @@ __device__ __forceinline__ void adam_one(const uint16_t* g, float* th, float* m,
     p[i] = (uint16_t)h;
 }
 
-// K3 (vector path).  All five arrays share the same element misalignment, so
+// K2 (vector path).  All five arrays share the same element misalignment, so
 // after `head` (0..3) scalar elements every array is aligned for 4-element
 // vectors: 16-byte fp32 and 8-byte fp16 accesses, consecutive lanes on
-// consecutive vectors.  Each thread handles U vectors per tile, loading all of
-// them before computing.  Elements [head + 4*nvec, n) are the tail (0..3).
-template <int U>
-__global__ __launch_bounds__(kAdamBlock) void k_adam_vec(const uint16_t* __restrict__ g, float* __restrict__ th,
-                                                         float* __restrict__ m, float* __restrict__ v,
-                                                         uint16_t* __restrict__ p, int64_t n, int64_t head,
-                                                         int64_t nvec, const Result* __restrict__ res,
-                                                         AdamConst c) {
+// consecutive vectors.  A tile is BLOCK*U vectors; each thread loads its U
+// vectors of all four inputs before computing.  Elements [head + 4*nvec, n)
+// are the tail (0..3).  Any grid size is valid (tiles are strided by it).
+template <int BLOCK, int U, bool NTL, bool NTS, bool XCD, bool REV>
+__global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__ g, float* __restrict__ th,
+                                                    float* __restrict__ m, float* __restrict__ v,
+                                                    uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec,
+                                                    const Result* __restrict__ res, AdamConst c) {
     if (res->skip)
         return;
     const float mult = res->mult;
@@ -237,24 +294,25 @@ __global__ __launch_bounds__(kAdamBlock) void k_adam_vec(const uint16_t* __restr
     f32x4* __restrict__ mv = reinterpret_cast<f32x4*>(m + head);
     f32x4* __restrict__ vv = reinterpret_cast<f32x4*>(v + head);
     u32x2* __restrict__ pv = reinterpret_cast<u32x2*>(p + head);
-    const int64_t tile = (int64_t)kAdamBlock * U;
-    const int64_t stride = (int64_t)gridDim.x * tile;
-    for (int64_t base = (int64_t)blockIdx.x * tile + threadIdx.x; base < nvec; base += stride) {
+    const int64_t tile = (int64_t)BLOCK * U;
+    const int64_t ntiles = (nvec + tile - 1) / tile;
+    for (int64_t tb = logical_block<XCD>(); tb < ntiles; tb += gridDim.x) {
+        const int64_t base = (REV ? ntiles - 1 - tb : tb) * tile + threadIdx.x;
         u32x2 gq[U];
         f32x4 tq[U], mq[U], vq[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t i = base + (int64_t)u * kAdamBlock;
+            const int64_t i = base + (int64_t)u * BLOCK;
             if (i < nvec) {
-                gq[u] = __builtin_nontemporal_load(gv + i);
-                tq[u] = __builtin_nontemporal_load(tv + i);
-                mq[u] = __builtin_nontemporal_load(mv + i);
-                vq[u] = __builtin_nontemporal_load(vv + i);
+                gq[u] = ld<NTL>(gv + i);
+                tq[u] = ld<NTL>(tv + i);
+                mq[u] = ld<NTL>(mv + i);
+                vq[u] = ld<NTL>(vv + i);
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int64_t i = base + (int64_t)u * kAdamBlock;
+            const int64_t i = base + (int64_t)u * BLOCK;
             if (i < nvec) {
                 float t[4] = {tq[u].x, tq[u].y, tq[u].z, tq[u].w};
                 float mm[4] = {mq[u].x, mq[u].y, mq[u].z, mq[u].w};
@@ -268,34 +326,52 @@ __global__ __launch_bounds__(kAdamBlock) void k_adam_vec(const uint16_t* __restr
                 const f32x4 mo = {mm[0], mm[1], mm[2], mm[3]};
                 const f32x4 vo = {vvv[0], vvv[1], vvv[2], vvv[3]};
                 const u32x2 po = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
-                __builtin_nontemporal_store(to, tv + i);
-                __builtin_nontemporal_store(mo, mv + i);
-                __builtin_nontemporal_store(vo, vv + i);
-                __builtin_nontemporal_store(po, pv + i);
+                st<NTS>(to, tv + i);
+                st<NTS>(mo, mv + i);
+                st<NTS>(vo, vv + i);
+                st<NTS>(po, pv + i);
             }
         }
     }
 }
 
-// K3 (scalar path) for arrays whose element misalignments differ.
-__global__ __launch_bounds__(kAdamBlock) void k_adam_scalar(const uint16_t* __restrict__ g, float* __restrict__ th,
-                                                            float* __restrict__ m, float* __restrict__ v,
-                                                            uint16_t* __restrict__ p, int64_t n,
-                                                            const Result* __restrict__ res, AdamConst c) {
+// K2 (scalar path) for arrays whose element misalignments differ.
+__global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(const uint16_t* __restrict__ g,
+                                                              float* __restrict__ th, float* __restrict__ m,
+                                                              float* __restrict__ v, uint16_t* __restrict__ p,
+                                                              int64_t n, const Result* __restrict__ res,
+                                                              AdamConst c) {
     if (res->skip)
         return;
     const float mult = res->mult;
-    const int64_t stride = (int64_t)gridDim.x * kAdamBlock;
-    for (int64_t i = (int64_t)blockIdx.x * kAdamBlock + threadIdx.x; i < n; i += stride)
+    const int64_t stride = (int64_t)gridDim.x * kScalarBlock;
+    for (int64_t i = (int64_t)blockIdx.x * kScalarBlock + threadIdx.x; i < n; i += stride)
         adam_one(g, th, m, v, p, i, mult, c);
 }
 
-// Streaming copy of nvec 16-byte vectors (bandwidth reference).
-__global__ __launch_bounds__(256) void k_probe_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
-                                                    int64_t nvec) {
-    const int64_t stride = (int64_t)gridDim.x * 256;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nvec; i += stride)
-        __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+// Streaming copy of nvec 16-byte vectors: the achievable-bandwidth reference
+// for the update kernel (same tiling knobs) and the calibration kernel for
+// hardware byte counters.
+template <int BLOCK, int U, bool NTL, bool NTS, bool XCD>
+__global__ __launch_bounds__(BLOCK) void k_probe_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
+                                                      int64_t nvec) {
+    const int64_t tile = (int64_t)BLOCK * U;
+    const int64_t stride = (int64_t)gridDim.x * tile;
+    for (int64_t base = logical_block<XCD>() * tile + threadIdx.x; base < nvec; base += stride) {
+        u32x4 q[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * BLOCK;
+            if (i < nvec)
+                q[u] = ld<NTL>(src + i);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * BLOCK;
+            if (i < nvec)
+                st<NTS>(q[u], dst + i);
+        }
+    }
 }
 
 }  // namespace zs

@@ -12,6 +12,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <algorithm>
 #include <map>
 #include <memory>
 #include <mutex>
@@ -49,7 +50,20 @@ int fail(int code, const char* fmt, ...) {
 // Launch planning.  One function decides every launch shape from n, so tests
 // and benchmarks exercise the same configuration.
 // ---------------------------------------------------------------------------
-constexpr int kAdamUnroll = 2;
+// Production launch policy of the streaming kernels (template knobs in
+// shard_kernels.hpp), chosen by measurement on MI355X in the two-kernel step
+// flow.  The HBM efficiency of these streams peaks well below full occupancy,
+// so the statistics pass (persistent grid) and the update (one tile per
+// workgroup) are launched with an LDS reservation that caps resident
+// workgroups per CU.  The statistics pass uses cache-allocating loads, which
+// leaves part of the gradient in the Infinity Cache for the update.
+constexpr int kStatsBlock = 64, kStatsUnroll = 4, kStatsPerCU = 8;
+constexpr bool kStatsNTL = false, kStatsXCD = false;
+constexpr int kAdamBlock = 64, kAdamUnroll = 1, kAdamPerCU = 12;
+constexpr bool kAdamNTL = true, kAdamNTS = true, kAdamXCD = false, kAdamREV = false;
+constexpr int64_t kAdamMaxBlocks = 1 << 26;
+constexpr int kCopyBlock = 64, kCopyUnroll = 1;
+constexpr bool kCopyNTL = true, kCopyNTS = true, kCopyXCD = false;
 
 struct Plan {
     int64_t ghead, gvec;   // statistics: unaligned head elements, 8-element vectors
@@ -61,15 +75,17 @@ struct Plan {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* v, const uint16_t* p, int64_t n) {
+Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* v, const uint16_t* p, int64_t n,
+               int ncu) {
     Plan pl{};
-    // statistics: 16-byte vectors of the gradient
+    // statistics: 16-byte vectors of the gradient, at most kStatsPerCU workgroups per CU
     const uintptr_t ga = reinterpret_cast<uintptr_t>(g);
     int64_t gh = (int64_t)(((16 - (ga & 15)) & 15) / 2);
     pl.ghead = gh < n ? gh : n;
     pl.gvec = (n - pl.ghead) / 8;
-    int64_t sb = ceil_div(pl.gvec, (int64_t)zs::kStatsBlock * zs::kStatsUnroll);
-    pl.stats_blocks = (int)(sb < 1 ? 1 : (sb > zs::kMaxStatsBlocks ? zs::kMaxStatsBlocks : sb));
+    int64_t sb = ceil_div(pl.gvec, (int64_t)kStatsBlock * kStatsUnroll);
+    const int64_t scap = std::min<int64_t>((int64_t)ncu * kStatsPerCU, zs::kMaxStatsBlocks);
+    pl.stats_blocks = (int)(sb < 1 ? 1 : (sb > scap ? scap : sb));
     // update: 4-element vectors (16-byte fp32, 8-byte fp16) need one common misalignment
     const int64_t ef[3] = {(int64_t)((reinterpret_cast<uintptr_t>(th) & 15) / 4),
                            (int64_t)((reinterpret_cast<uintptr_t>(m) & 15) / 4),
@@ -81,14 +97,22 @@ Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* 
         int64_t h = (4 - ef[0]) & 3;
         pl.head = h < n ? h : n;
         pl.nvec = (n - pl.head) / 4;
-        int64_t ab = ceil_div(pl.nvec, (int64_t)zs::kAdamBlock * kAdamUnroll);
-        pl.adam_blocks = ab < 1 ? 1 : (ab > (1 << 20) ? (1 << 20) : ab);
+        int64_t ab = ceil_div(pl.nvec, (int64_t)kAdamBlock * kAdamUnroll);
+        pl.adam_blocks = ab < 1 ? 1 : (ab > kAdamMaxBlocks ? kAdamMaxBlocks : ab);
     } else {
         pl.head = pl.nvec = 0;
-        int64_t ab = ceil_div(n, zs::kAdamBlock);
-        pl.adam_blocks = ab < 1 ? 1 : (ab > (1 << 20) ? (1 << 20) : ab);
+        int64_t ab = ceil_div(n, zs::kScalarBlock);
+        pl.adam_blocks = ab < 1 ? 1 : (ab > kAdamMaxBlocks ? kAdamMaxBlocks : ab);
     }
     return pl;
+}
+
+// Dynamic LDS that caps resident workgroups of a kernel at `per_cu` per CU
+// (a workgroup's LDS is its static LDS plus this reservation).
+size_t occupancy_lds(size_t lds_per_cu, size_t lds_per_block, int per_cu) {
+    size_t l = (lds_per_cu / (size_t)per_cu) & ~(size_t)511;
+    const size_t cap = lds_per_block > 1024 ? lds_per_block - 1024 : 0;  // room for static LDS
+    return l > cap ? cap : l;
 }
 
 // ---------------------------------------------------------------------------
@@ -96,10 +120,14 @@ Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* 
 // ---------------------------------------------------------------------------
 struct Ctx {
     std::mutex mu;
-    zs::Partial* part = nullptr;   // kMaxStatsBlocks partial records (device)
-    zs::Result* res = nullptr;     // result record (device)
-    zs::Result* host = nullptr;    // pinned host copy of the result record
-    hipEvent_t flag_ev = nullptr;  // recorded after the result copy
+    zs::Partial* part = nullptr;    // kMaxStatsBlocks partial records (device)
+    zs::Result* res = nullptr;      // result record (device), read by the update kernel
+    zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
+    zs::Result* host_dev = nullptr; // its device-side address
+    hipEvent_t flag_ev = nullptr;   // recorded after the finalize kernel
+    uint32_t seq = 0;               // call counter echoed in the result record
+    int ncu = 0;
+    size_t stats_lds = 0, adam_lds = 0;
 };
 
 std::mutex g_ctx_mu;
@@ -115,11 +143,19 @@ int get_ctx(hipStream_t stream, Ctx** out) {
         *out = it->second.get();
         return 0;
     }
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev));
     std::unique_ptr<Ctx> c(new Ctx);
-    if (hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) != hipSuccess ||
-        hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) != hipSuccess ||
-        hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result), hipHostMallocDefault) != hipSuccess ||
-        hipEventCreateWithFlags(&c->flag_ev, hipEventDisableTiming) != hipSuccess) {
+    c->ncu = prop.multiProcessorCount;
+    c->stats_lds = occupancy_lds(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock, kStatsPerCU);
+    c->adam_lds = occupancy_lds(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock, kAdamPerCU);
+    bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
+              hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
+                            hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess &&
+              hipEventCreateWithFlags(&c->flag_ev, hipEventDisableTiming) == hipSuccess;
+    if (!ok) {
         if (c->part) (void)hipFree(c->part);
         if (c->res) (void)hipFree(c->res);
         if (c->host) (void)hipHostFree(c->host);
@@ -127,6 +163,7 @@ int get_ctx(hipStream_t stream, Ctx** out) {
         (void)hipGetLastError();
         return fail(ZERO_ENOMEM, "could not allocate the step workspace on device %d", dev);
     }
+    std::memset(c->host, 0, sizeof(zs::Result));
     *out = c.get();
     g_ctx.emplace(key, std::move(c));
     return 0;
@@ -136,7 +173,7 @@ int get_ctx(hipStream_t stream, Ctx** out) {
 // Profiling: events around the statistics and update kernels of each step.
 // ---------------------------------------------------------------------------
 struct ProfRec {
-    hipEvent_t e[4];
+    hipEvent_t e[3];  // before statistics, between the kernels, after the update
 };
 
 std::mutex g_prof_mu;
@@ -159,10 +196,10 @@ hipEvent_t prof_event() {
 
 int prof_drain_locked() {
     for (ProfRec& r : g_prof_pending) {
-        HIP_TRY(hipEventSynchronize(r.e[3]));
+        HIP_TRY(hipEventSynchronize(r.e[2]));
         float a = 0.f, b = 0.f;
         HIP_TRY(hipEventElapsedTime(&a, r.e[0], r.e[1]));
-        HIP_TRY(hipEventElapsedTime(&b, r.e[2], r.e[3]));
+        HIP_TRY(hipEventElapsedTime(&b, r.e[1], r.e[2]));
         g_prof_acc.steps += 1;
         g_prof_acc.stats_ms += a;
         g_prof_acc.update_ms += b;
@@ -314,7 +351,8 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     c.eps = (float)eps;
     c.wd = (float)weight_decay;
 
-    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n);
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    const uint32_t seq = ++ctx->seq;
 
     ProfRec pr{};
     bool prof = false;
@@ -330,25 +368,25 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
 
     if (prof)
         HIP_TRY(hipEventRecord(pr.e[0], stream));
-    zs::k_stats<<<pl.stats_blocks, zs::kStatsBlock, 0, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+    zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
+        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
     HIP_TRY(hipGetLastError());
-    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, loss_scale, clip);
+    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, ctx->host_dev,
+                                                      loss_scale, clip, seq);
     HIP_TRY(hipGetLastError());
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[1], stream));
-    HIP_TRY(hipMemcpyAsync(ctx->host, ctx->res, sizeof(zs::Result), hipMemcpyDeviceToHost, stream));
     HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
     if (prof)
-        HIP_TRY(hipEventRecord(pr.e[2], stream));
+        HIP_TRY(hipEventRecord(pr.e[1], stream));
     if (pl.vec)
-        zs::k_adam_vec<kAdamUnroll><<<(unsigned)pl.adam_blocks, zs::kAdamBlock, 0, stream>>>(
-            grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
+        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>
+            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
     else
-        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kAdamBlock, 0, stream>>>(
+        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
             grad16, master32, m32, v32, param16_out, n, ctx->res, c);
     HIP_TRY(hipGetLastError());
     if (prof) {
-        HIP_TRY(hipEventRecord(pr.e[3], stream));
+        HIP_TRY(hipEventRecord(pr.e[2], stream));
         std::lock_guard<std::mutex> plk(g_prof_mu);
         g_prof_pending.push_back(pr);
         if (g_prof_pending.size() >= 4096) {
@@ -357,9 +395,12 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
                 return r2;
         }
     }
-    // The update kernel is already queued behind the copy: wait only for the flag.
+    // The update kernel is already queued: wait only for the statistics and finalize kernels.
     HIP_TRY(hipEventSynchronize(ctx->flag_ev));
-    const zs::Result r = *ctx->host;
+    zs::Result r;
+    std::memcpy(&r, (const void*)ctx->host, sizeof r);
+    if (r.seq != seq)
+        return fail(ZERO_EHIP, "zero_shard_step: result record not published (seq %u, expected %u)", r.seq, seq);
     t_stats.sumsq = r.sumsq;
     t_stats.norm = r.norm;
     t_stats.coef = r.coef;
@@ -399,9 +440,10 @@ int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {
     if (bytes == 0)
         return ZERO_OK;
     const int64_t nvec = bytes / 16;
-    int64_t blocks = ceil_div(nvec, 256 * 4);
-    blocks = blocks < 1 ? 1 : (blocks > (1 << 20) ? (1 << 20) : blocks);
-    zs::k_probe_copy<<<(unsigned)blocks, 256, 0, reinterpret_cast<hipStream_t>(stream_)>>>(
+    int64_t blocks = ceil_div(nvec, (int64_t)kCopyBlock * kCopyUnroll);
+    blocks = blocks < 1 ? 1 : (blocks > kAdamMaxBlocks ? kAdamMaxBlocks : blocks);
+    zs::k_probe_copy<kCopyBlock, kCopyUnroll, kCopyNTL, kCopyNTS, kCopyXCD>
+        <<<(unsigned)blocks, kCopyBlock, 0, reinterpret_cast<hipStream_t>(stream_)>>>(
         reinterpret_cast<const zs::u32x4*>(src), reinterpret_cast<zs::u32x4*>(dst), nvec);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
