@@ -33,10 +33,15 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_1910_02054_amd", "csrc", f) for f in
 
 
 def kernel_source_hash() -> str:
+    """Hash of the kernels' source and of the production launch policy (the block of
+    zero_shard.hip that fixes block sizes, unrolls, cache policies and occupancy caps)."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+    with open(KERNEL_SOURCES[0], "rb") as f:
+        h.update(f.read())
+    with open(KERNEL_SOURCES[1]) as f:
+        host = f.read()
+    a, b = host.index("// Production launch policy"), host.index("struct Plan {")
+    h.update(host[a:b].encode())
     return h.hexdigest()[:16]
 
 

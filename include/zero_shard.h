@@ -107,6 +107,36 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
                     int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
                     int64_t step, double loss_scale, double clip, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Split-phase step: local statistics, then the update with global ones      */
+/* ------------------------------------------------------------------------ */
+
+/* With N_d ranks (Sec. 5.1-5.2) clipping and the skip decision need the norm
+ * of the WHOLE gradient, so each rank first computes its shard's local sum of
+ * squares, the ranks combine the N_d values (an all-reduce of 8 bytes per
+ * rank; summing them in rank order gives every rank the same bits), and each
+ * rank then applies the update with the global value.  zero_shard_step is the
+ * one-rank composition of the two phases.
+ *
+ * zero_shard_stats: *local_sumsq = sum of grad16^2 over [0, n) (loss-scaled,
+ * accumulated in fp64; +inf or NaN iff some element is inf or NaN).  Blocks
+ * until the value is known.  n == 0 gives 0.  grad16: device, 2-byte aligned,
+ * read only.  Returns 0 or ZERO_E*. */
+int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, void* stream);
+
+/* zero_shard_apply: the update of zero_shard_step with the global sum of
+ * squares supplied by the caller (the sum over all ranks of their
+ * local_sumsq).  Overflow = global_sumsq is not finite: then nothing is
+ * written and ZERO_SKIPPED is returned.  Otherwise norm =
+ * sqrt(global_sumsq)/loss_scale and the rest is exactly zero_shard_step's
+ * update (same kernels).  Arguments and errors as for zero_shard_step;
+ * global_sumsq must not be negative.  Does not block: the skip decision is
+ * known on the host from global_sumsq, and the kernels are queued on
+ * `stream`.  Does not change zero_shard_last_stats. */
+int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                     int64_t n, double global_sumsq, double lr, double beta1, double beta2, double eps,
+                     double weight_decay, int64_t step, double loss_scale, double clip, void* stream);
+
 /* Statistics of the calling thread's last successful zero_shard_step. */
 typedef struct {
     double sumsq;     /* sum of grad16^2 (loss-scaled), accumulated in fp64;

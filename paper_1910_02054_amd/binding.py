@@ -48,6 +48,8 @@ class Profile(ctypes.Structure):
 _P, _i64, _i32, _dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
 _lib.zero_partition_layout.argtypes = [_i64, _i32, _i32, ctypes.POINTER(Layout)]
 _lib.zero_shard_step.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
+_lib.zero_shard_stats.argtypes = [_P, _i64, ctypes.POINTER(_dbl), _P]
+_lib.zero_shard_apply.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
 _lib.zero_shard_last_stats.argtypes = [ctypes.POINTER(StepStats)]
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
@@ -57,12 +59,14 @@ _lib.zero_last_error.restype = ctypes.c_char_p
 _lib.zero_profile_enable.argtypes = [_i32]
 _lib.zero_profile_read.argtypes = [ctypes.POINTER(Profile)]
 _lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
-for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_last_stats", "zero_scaler_init",
+for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
+           "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
            "zero_probe_copy"):
     getattr(_lib, _f).restype = ctypes.c_int
 
-EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_last_stats", "zero_scaler_init",
+EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
+           "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
            "zero_profile_read", "zero_probe_copy")
 
@@ -121,6 +125,35 @@ def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, e
         _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(lr), float(beta1),
         float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
+        _stream(stream)))
+
+
+def zero_shard_stats(grad16, n=None, stream=None) -> float:
+    """Local sum of squares of a shard's loss-scaled fp16 gradients (fp64; inf/NaN on overflow)."""
+    import torch
+    if n is None:
+        n = grad16.numel()
+    out = ctypes.c_double()
+    _check(_lib.zero_shard_stats(_addr(grad16, (torch.float16, torch.int16), "grad16"), int(n), ctypes.byref(out),
+                                 _stream(stream)))
+    return out.value
+
+
+def zero_shard_apply(grad16, master32, m32, v32, param16_out, global_sumsq, lr, beta1, beta2, eps, weight_decay,
+                     step, loss_scale, clip, n=None, stream=None) -> int:
+    """The update with a caller-supplied global sum of squares; 0 applied, 1 skipped."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    if n is None:
+        n = grad16.numel()
+        for t in (master32, m32, v32, param16_out):
+            if t.numel() != n:
+                raise ValueError("shard tensors differ in length")
+    return _check(_lib.zero_shard_apply(
+        _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(global_sumsq), float(lr),
+        float(beta1), float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
         _stream(stream)))
 
 

@@ -237,6 +237,14 @@ __global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restr
     }
 }
 
+// Result record from a global sum of squares supplied by the caller (the
+// split-phase step: each rank's local sums combined outside the library).
+__global__ __launch_bounds__(64) void k_set_result(Result* __restrict__ res, double global_sumsq, double loss_scale,
+                                                   double clip, uint32_t seq) {
+    if (threadIdx.x == 0)
+        *res = make_result(global_sumsq, loss_scale, clip, seq);
+}
+
 // ---------------------------------------------------------------------------
 // The per-element update: one definition for the vector body, the unaligned
 // head/tail and the scalar path, so every element is computed identically.

@@ -214,6 +214,118 @@ bool is_fin(double x) { return std::isfinite(x); }
 
 bool overlaps(uintptr_t a, size_t an, uintptr_t b, size_t bn) { return a < b + bn && b < a + an; }
 
+constexpr int64_t kMaxNumel = (int64_t)1 << 40;
+
+// Argument checks shared by zero_shard_step and zero_shard_apply; nothing is
+// launched unless every check passes.
+int check_update_args(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
+                      const float* v32, const uint16_t* param16_out, int64_t n, double lr, double beta1,
+                      double beta2, double eps, double weight_decay, int64_t step, double loss_scale, double clip) {
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "%s: n=%lld outside [0, 2^40]", fn, (long long)n);
+    if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
+        return fail(ZERO_EINVAL, "%s: need finite lr >= 0, eps >= 0, weight_decay", fn);
+    if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+        return fail(ZERO_EINVAL, "%s: beta1, beta2 must lie in [0, 1)", fn);
+    if (step < 1)
+        return fail(ZERO_EINVAL, "%s: step (t) must be >= 1, got %lld", fn, (long long)step);
+    if (!is_fin(loss_scale) || !(loss_scale > 0.0))
+        return fail(ZERO_EINVAL, "%s: loss_scale must be finite and > 0", fn);
+    if (std::isnan(clip))
+        return fail(ZERO_EINVAL, "%s: clip is NaN", fn);
+    if (n > 0) {
+        if (!grad16 || !master32 || !m32 || !v32 || !param16_out)
+            return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
+        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
+                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
+                                reinterpret_cast<uintptr_t>(param16_out)};
+        const size_t sz[5] = {2, 4, 4, 4, 2};
+        for (int i = 0; i < 5; ++i)
+            if (a[i] % sz[i])
+                return fail(ZERO_EINVAL, "%s: array %d is not %zu-byte aligned", fn, i, sz[i]);
+        for (int i = 0; i < 5; ++i)
+            for (int j = i + 1; j < 5; ++j)
+                if (overlaps(a[i], sz[i] * (size_t)n, a[j], sz[j] * (size_t)n))
+                    return fail(ZERO_EINVAL, "%s: arrays %d and %d overlap", fn, i, j);
+    }
+    return ZERO_OK;
+}
+
+// fp32 constants, each computed in double and rounded once (the bias
+// corrections 1 - beta^t use the C library's pow).
+zs::AdamConst adam_const(double lr, double beta1, double beta2, double eps, double wd, int64_t step) {
+    zs::AdamConst c;
+    c.lr = (float)lr;
+    c.b1 = (float)beta1;
+    c.omb1 = (float)(1.0 - beta1);
+    c.b2 = (float)beta2;
+    c.omb2 = (float)(1.0 - beta2);
+    c.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
+    c.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
+    c.eps = (float)eps;
+    c.wd = (float)wd;
+    return c;
+}
+
+// Statistics + finalize: the result record lands in ctx->res and ctx->host.
+int launch_stats(Ctx* ctx, const uint16_t* grad16, int64_t n, const Plan& pl, double loss_scale, double clip,
+                 uint32_t seq, hipStream_t stream) {
+    zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
+        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+    HIP_TRY(hipGetLastError());
+    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, ctx->host_dev,
+                                                      loss_scale, clip, seq);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+// The fused update reading its scalars from ctx->res.
+int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                  int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream) {
+    if (pl.vec)
+        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>
+            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
+    else
+        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
+            grad16, master32, m32, v32, param16_out, n, ctx->res, c);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+// Wait for the event recorded after the finalize kernel and read the mapped record.
+int read_result(Ctx* ctx, uint32_t seq, zs::Result* out) {
+    HIP_TRY(hipEventSynchronize(ctx->flag_ev));
+    std::memcpy(out, (const void*)ctx->host, sizeof *out);
+    if (out->seq != seq)
+        return fail(ZERO_EHIP, "result record not published (seq %u, expected %u)", out->seq, seq);
+    return ZERO_OK;
+}
+
+// Profiling events of one step (taken from a pool while profiling is on).
+bool prof_begin(ProfRec* pr) {
+    std::lock_guard<std::mutex> plk(g_prof_mu);
+    if (!g_prof_on)
+        return false;
+    for (hipEvent_t& e : pr->e)
+        e = prof_event();
+    if (!pr->e[0] || !pr->e[1] || !pr->e[2]) {
+        for (hipEvent_t e : pr->e)
+            if (e)
+                g_prof_pool.push_back(e);
+        pr->e[0] = nullptr;
+    }
+    return true;
+}
+
+int prof_end(const ProfRec& pr) {
+    std::lock_guard<std::mutex> plk(g_prof_mu);
+    g_prof_pending.push_back(pr);
+    if (g_prof_pending.size() >= 4096)
+        return prof_drain_locked();
+    return ZERO_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -298,109 +410,46 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
                     int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
                     int64_t step, double loss_scale, double clip, void* stream_) {
     // ---- argument checks: nothing is launched unless all pass ----
-    if (n < 0 || n > ((int64_t)1 << 40))
-        return fail(ZERO_EINVAL, "zero_shard_step: n=%lld outside [0, 2^40]", (long long)n);
-    if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
-        return fail(ZERO_EINVAL, "zero_shard_step: need finite lr >= 0, eps >= 0, weight_decay");
-    if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
-        return fail(ZERO_EINVAL, "zero_shard_step: beta1, beta2 must lie in [0, 1)");
-    if (step < 1)
-        return fail(ZERO_EINVAL, "zero_shard_step: step (t) must be >= 1, got %lld", (long long)step);
-    if (!is_fin(loss_scale) || !(loss_scale > 0.0))
-        return fail(ZERO_EINVAL, "zero_shard_step: loss_scale must be finite and > 0");
-    if (std::isnan(clip))
-        return fail(ZERO_EINVAL, "zero_shard_step: clip is NaN");
-    if (n > 0) {
-        if (!grad16 || !master32 || !m32 || !v32 || !param16_out)
-            return fail(ZERO_EINVAL, "zero_shard_step: NULL array with n > 0");
-        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
-                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
-                                reinterpret_cast<uintptr_t>(param16_out)};
-        const size_t sz[5] = {2, 4, 4, 4, 2};
-        for (int i = 0; i < 5; ++i)
-            if (a[i] % sz[i])
-                return fail(ZERO_EINVAL, "zero_shard_step: array %d is not %zu-byte aligned", i, sz[i]);
-        for (int i = 0; i < 5; ++i)
-            for (int j = i + 1; j < 5; ++j)
-                if (overlaps(a[i], sz[i] * (size_t)n, a[j], sz[j] * (size_t)n))
-                    return fail(ZERO_EINVAL, "zero_shard_step: arrays %d and %d overlap", i, j);
-    }
+    int rc = check_update_args("zero_shard_step", grad16, master32, m32, v32, param16_out, n, lr, beta1, beta2, eps,
+                               weight_decay, step, loss_scale, clip);
+    if (rc)
+        return rc;
     if (n == 0) {
         t_stats = zero_step_stats_t{0.0, 0.0, 1.0, (float)(1.0 / loss_scale), 0, 0, 0, 0};
         t_have_stats = true;
         return ZERO_OK;
     }
-
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
     Ctx* ctx = nullptr;
-    int rc = get_ctx(stream, &ctx);
-    if (rc)
+    if ((rc = get_ctx(stream, &ctx)))
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
-
-    // fp32 constants, each computed in double and rounded once (the bias
-    // corrections 1 - beta^t use the C library's pow).
-    zs::AdamConst c;
-    c.lr = (float)lr;
-    c.b1 = (float)beta1;
-    c.omb1 = (float)(1.0 - beta1);
-    c.b2 = (float)beta2;
-    c.omb2 = (float)(1.0 - beta2);
-    c.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
-    c.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
-    c.eps = (float)eps;
-    c.wd = (float)weight_decay;
-
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
     const uint32_t seq = ++ctx->seq;
 
     ProfRec pr{};
-    bool prof = false;
-    {
-        std::lock_guard<std::mutex> plk(g_prof_mu);
-        if (g_prof_on) {
-            prof = true;
-            for (hipEvent_t& e : pr.e)
-                if (!(e = prof_event()))
-                    return fail(ZERO_EHIP, "zero_shard_step: could not create a profiling event");
-        }
-    }
-
+    const bool prof = prof_begin(&pr);
+    if (prof && !pr.e[0])
+        return fail(ZERO_EHIP, "zero_shard_step: could not create a profiling event");
     if (prof)
         HIP_TRY(hipEventRecord(pr.e[0], stream));
-    zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
-        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
-    HIP_TRY(hipGetLastError());
-    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, ctx->host_dev,
-                                                      loss_scale, clip, seq);
-    HIP_TRY(hipGetLastError());
+    if ((rc = launch_stats(ctx, grad16, n, pl, loss_scale, clip, seq, stream)))
+        return rc;
     HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
     if (prof)
         HIP_TRY(hipEventRecord(pr.e[1], stream));
-    if (pl.vec)
-        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>
-            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
-                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
-    else
-        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
-            grad16, master32, m32, v32, param16_out, n, ctx->res, c);
-    HIP_TRY(hipGetLastError());
+    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
+        return rc;
     if (prof) {
         HIP_TRY(hipEventRecord(pr.e[2], stream));
-        std::lock_guard<std::mutex> plk(g_prof_mu);
-        g_prof_pending.push_back(pr);
-        if (g_prof_pending.size() >= 4096) {
-            int r2 = prof_drain_locked();
-            if (r2)
-                return r2;
-        }
+        if ((rc = prof_end(pr)))
+            return rc;
     }
     // The update kernel is already queued: wait only for the statistics and finalize kernels.
-    HIP_TRY(hipEventSynchronize(ctx->flag_ev));
     zs::Result r;
-    std::memcpy(&r, (const void*)ctx->host, sizeof r);
-    if (r.seq != seq)
-        return fail(ZERO_EHIP, "zero_shard_step: result record not published (seq %u, expected %u)", r.seq, seq);
+    if ((rc = read_result(ctx, seq, &r)))
+        return rc;
     t_stats.sumsq = r.sumsq;
     t_stats.norm = r.norm;
     t_stats.coef = r.coef;
@@ -411,6 +460,60 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     t_stats.n = n;
     t_have_stats = true;
     return r.skip ? ZERO_SKIPPED : ZERO_OK;
+}
+
+int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, void* stream_) {
+    if (!local_sumsq)
+        return fail(ZERO_EINVAL, "zero_shard_stats: NULL local_sumsq");
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "zero_shard_stats: n=%lld outside [0, 2^40]", (long long)n);
+    if (n > 0 && (!grad16 || reinterpret_cast<uintptr_t>(grad16) % 2))
+        return fail(ZERO_EINVAL, "zero_shard_stats: grad16 is NULL or not 2-byte aligned");
+    if (n == 0) {
+        *local_sumsq = 0.0;
+        return ZERO_OK;
+    }
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    int rc = get_ctx(stream, &ctx);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
+    const uint32_t seq = ++ctx->seq;
+    if ((rc = launch_stats(ctx, grad16, n, pl, 1.0, 0.0, seq, stream)))
+        return rc;
+    HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
+    zs::Result r;
+    if ((rc = read_result(ctx, seq, &r)))
+        return rc;
+    *local_sumsq = r.sumsq;
+    return ZERO_OK;
+}
+
+int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                     int64_t n, double global_sumsq, double lr, double beta1, double beta2, double eps,
+                     double weight_decay, int64_t step, double loss_scale, double clip, void* stream_) {
+    int rc = check_update_args("zero_shard_apply", grad16, master32, m32, v32, param16_out, n, lr, beta1, beta2, eps,
+                               weight_decay, step, loss_scale, clip);
+    if (rc)
+        return rc;
+    if (global_sumsq < 0.0)
+        return fail(ZERO_EINVAL, "zero_shard_apply: global_sumsq is negative");
+    const bool overflow = !is_fin(global_sumsq);
+    if (n == 0 || overflow)
+        return overflow ? ZERO_SKIPPED : ZERO_OK;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    const uint32_t seq = ++ctx->seq;
+    zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
+    HIP_TRY(hipGetLastError());
+    return launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
 }
 
 int zero_profile_enable(int32_t on) {

@@ -129,3 +129,39 @@ def test_step_with_zero_elements_is_a_noop(zb):
     assert _step_raw(zb, [0, 0, 0, 0, 0], 0) == zb.ZERO_OK
     st = zb.zero_shard_last_stats()
     assert st.n == 0 and st.skipped == 0
+
+
+def _apply_raw(zb, ptrs, n, gsum, **kw):
+    args = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0, step=1, scale=65536.0, clip=1.0)
+    args.update(kw)
+    return zb.raw_library().zero_shard_apply(*ptrs, n, gsum, args["lr"], args["beta1"], args["beta2"], args["eps"],
+                                             args["wd"], args["step"], args["scale"], args["clip"], None)
+
+
+@pytest.mark.parametrize("kw,ptrs,n,gsum", [
+    (dict(), GOOD, -1, 1.0),
+    (dict(), [0] + GOOD[1:], 10, 1.0),
+    (dict(), [GOOD[0], GOOD[1], GOOD[1] + 8] + GOOD[3:], 10, 1.0),
+    (dict(step=0), GOOD, 10, 1.0),
+    (dict(scale=-2.0), GOOD, 10, 1.0),
+    (dict(), GOOD, 10, -1.0),
+])
+def test_apply_rejects_invalid_arguments(zb, kw, ptrs, n, gsum):
+    assert _apply_raw(zb, ptrs, n, gsum, **kw) == zb.ZERO_EINVAL
+
+
+def test_apply_overflow_and_empty_need_no_gpu(zb):
+    # a non-finite global sum is the skip decision itself: nothing is launched
+    assert _apply_raw(zb, GOOD, 10, float("inf")) == zb.ZERO_SKIPPED
+    assert _apply_raw(zb, GOOD, 10, float("nan")) == zb.ZERO_SKIPPED
+    assert _apply_raw(zb, [0, 0, 0, 0, 0], 0, 1.0) == zb.ZERO_OK
+
+
+def test_stats_rejects_invalid_arguments(zb):
+    lib = zb.raw_library()
+    out = ctypes.c_double(7.0)
+    assert lib.zero_shard_stats(None, 10, ctypes.byref(out), None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_stats(GOOD[0] + 1, 10, ctypes.byref(out), None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_stats(GOOD[0], -3, ctypes.byref(out), None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_stats(GOOD[0], 10, None, None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_stats(None, 0, ctypes.byref(out), None) == zb.ZERO_OK and out.value == 0.0

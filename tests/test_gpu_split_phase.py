@@ -1,0 +1,168 @@
+"""GPU tests of the split-phase step (local statistics -> global sum -> update).
+
+N_d ranks are emulated on one GPU: each rank's shard is a view at its real
+offset r*S into padded flat buffers (Sec. 5.1 layout, tail padding), its local
+sum of squares comes from zero_shard_stats, the host adds the N_d values in
+rank order (what an all-gather followed by an ordered sum gives every rank),
+and each rank applies the update with that global value.  Partition
+invariance: the concatenated shard updates equal one update of the whole flat
+range with the same global value, bit for bit; both agree with the oracle's
+unpartitioned step.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import gpu_harness as H  # noqa: E402
+
+import oracle  # noqa: E402
+from paper_1910_02054_amd import workloads  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+HP = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0)
+
+
+def say(*a):
+    print("[gpu-split]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    from paper_1910_02054_amd import binding
+    assert torch.cuda.is_available()
+    return torch, binding, torch.device("cuda:0")
+
+
+def _flat(env, psi, padded, g16, theta, m, v):
+    torch, zb, dev = env
+    bufs = [H.Guarded(torch, padded, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                                       torch.float16)]
+    pad = padded - psi
+    # the padding carries its own canary; the step must never touch it
+    bufs[0].upload(np.concatenate([g16, np.full(pad, 0x7C00, np.uint16)]))  # inf in the padding: must not be read
+    for b, a in zip(bufs[1:4], (theta, m, v)):
+        b.upload(np.concatenate([a, np.full(pad, -7.0, np.float32)]))
+    bufs[4].upload(np.full(padded, workloads.P16_SENTINEL, np.uint16))
+    return bufs
+
+
+def test_split_equals_fused_step(env):
+    torch, zb, dev = env
+    n = 1_000_003
+    g16, theta, m, v = workloads.random_case(201, n)
+    a = [H.Guarded(torch, n, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                               torch.float16)]
+    b = [H.Guarded(torch, n, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                               torch.float16)]
+    for bufs in (a, b):
+        for buf, arr in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+            buf.upload(arr)
+    say("fused step vs stats+apply, n", n)
+    f1 = zb.zero_shard_step(*(x.view for x in a), HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], HP["weight_decay"],
+                            1, 2.0 ** 16, 1.0)
+    st = zb.zero_shard_last_stats()
+    local = zb.zero_shard_stats(b[0].view)
+    f2 = zb.zero_shard_apply(*(x.view for x in b), local, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
+                             HP["weight_decay"], 1, 2.0 ** 16, 1.0)
+    torch.cuda.synchronize()
+    assert f1 == f2 == 0 and local == st.sumsq
+    for x, y in zip(a[1:], b[1:]):
+        assert np.array_equal(x.download().view(np.uint8), y.download().view(np.uint8))
+    assert all(x.guards_intact() for x in a + b)
+
+
+@pytest.mark.parametrize("psi,nd", [(4_194_305, 4), (1_000_003, 7), (4_194_304, 4)])
+def test_partition_invariance_on_gpu(env, psi, nd):
+    torch, zb, dev = env
+    w = workloads.WORKLOADS["tiny"]
+    S, _, _, padded = oracle.layout(psi, nd, 0)
+    theta, m, v = workloads.initial_state(w, psi)
+    m += np.float32(1e-5)
+    v += np.float32(1e-9)
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(psi)]
+    g16 = workloads.gradients(w, psi, 1, w.loss_scale)
+    ranks = _flat(env, psi, padded, g16, theta, m, v)
+    whole = _flat(env, psi, padded, g16, theta, m, v)
+    shards = [zb.zero_partition_layout(psi, nd, r) for r in range(nd)]
+    say("partition invariance psi", psi, "nd", nd, "S", S)
+    local = []
+    for lay in shards:
+        sl = slice(lay.offset, lay.offset + lay.valid_numel)
+        local.append(zb.zero_shard_stats(ranks[0].view[sl]))
+    global_sumsq = 0.0
+    for x in local:  # rank order
+        global_sumsq += x
+    for t, lay in enumerate(shards):
+        sl = slice(lay.offset, lay.offset + lay.valid_numel)
+        f = zb.zero_shard_apply(*(b.view[sl] for b in ranks), global_sumsq, w.lr, w.beta1, w.beta2, w.eps, 0.01,
+                                1, w.loss_scale, w.clip)
+        assert f == 0
+    sl = slice(0, psi)
+    f = zb.zero_shard_apply(*(b.view[sl] for b in whole), global_sumsq, w.lr, w.beta1, w.beta2, w.eps, 0.01, 1,
+                            w.loss_scale, w.clip)
+    torch.cuda.synchronize()
+    assert f == 0
+    got_r = [b.download().copy() for b in ranks[1:]]
+    got_w = [b.download().copy() for b in whole[1:]]
+    for a, b in zip(got_r, got_w):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))  # bitwise partition invariance
+    # padding untouched
+    assert np.all(got_r[0][psi:] == np.float32(-7.0)) and np.all(got_r[3][psi:] == workloads.P16_SENTINEL)
+    assert all(b.guards_intact() for b in ranks + whole)
+    # against the oracle's unpartitioned step with exact statistics
+    skip, sc = H.oracle_step(g16, *ref, w.lr, w.beta1, w.beta2, w.eps, 0.01, 1, w.loss_scale, w.clip)
+    assert skip == 0 and abs(global_sumsq / sc.sumsq - 1) <= 1e-12
+    d = H.compare_state([x[:psi] for x in got_r], ref)
+    say(d)
+
+
+def test_overflow_on_one_rank_skips_every_rank(env):
+    torch, zb, dev = env
+    w = workloads.WORKLOADS["tiny"]
+    psi, nd = 400_003, 4
+    S, _, _, padded = oracle.layout(psi, nd, 0)
+    theta, m, v = workloads.initial_state(w, psi)
+    g16 = workloads.gradients(w, psi, 1, w.loss_scale)
+    bad = oracle.layout(psi, nd, 2)[1] + 17
+    g16[bad] = 0x7E00
+    bufs = _flat(env, psi, padded, g16, theta, m, v)
+    shards = [zb.zero_partition_layout(psi, nd, r) for r in range(nd)]
+    local = [zb.zero_shard_stats(bufs[0].view[l.offset:l.offset + l.valid_numel]) for l in shards]
+    assert [np.isfinite(x) for x in local] == [True, True, False, True]
+    g = sum(local)
+    flags = [zb.zero_shard_apply(*(b.view[l.offset:l.offset + l.valid_numel] for b in bufs), g, w.lr, w.beta1,
+                                 w.beta2, w.eps, 0.0, 1, w.loss_scale, w.clip) for l in shards]
+    torch.cuda.synchronize()
+    assert flags == [1, 1, 1, 1]
+    assert np.array_equal(bufs[1].download()[:psi], theta)
+    assert np.all(bufs[4].download() == workloads.P16_SENTINEL)
+
+
+def test_multi_step_ranks_follow_the_oracle(env):
+    torch, zb, dev = env
+    w = workloads.WORKLOADS["tiny"]
+    psi, nd = w.psi + 3, w.nd
+    S, _, _, padded = oracle.layout(psi, nd, 0)
+    theta, m, v = workloads.initial_state(w, psi)
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(psi)]
+    bufs = _flat(env, psi, padded, np.zeros(psi, np.uint16), theta, m, v)
+    shards = [zb.zero_partition_layout(psi, nd, r) for r in range(nd)]
+    for t in range(1, 4):
+        g16 = workloads.gradients(w, psi, t, w.loss_scale)
+        bufs[0].view[:psi].copy_(torch.from_numpy(g16.view(np.int16)).view(torch.float16))
+        local = [zb.zero_shard_stats(bufs[0].view[l.offset:l.offset + l.valid_numel]) for l in shards]
+        g = 0.0
+        for x in local:
+            g += x
+        for l in shards:
+            assert zb.zero_shard_apply(*(b.view[l.offset:l.offset + l.valid_numel] for b in bufs), g, w.lr, w.beta1,
+                                       w.beta2, w.eps, 0.0, t, w.loss_scale, w.clip) == 0
+        torch.cuda.synchronize()
+        skip, _ = H.oracle_step(g16, *ref, w.lr, w.beta1, w.beta2, w.eps, 0.0, t, w.loss_scale, w.clip)
+        assert skip == 0
+        d = H.compare_state([b.download()[:psi] for b in bufs[1:]], ref)
+        say("step", t, d)
