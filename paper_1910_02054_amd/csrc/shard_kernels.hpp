@@ -212,8 +212,9 @@ __global__ __launch_bounds__(BLOCK) void k_stats(const uint16_t* __restrict__ g,
 // ---------------------------------------------------------------------------
 // K2: finalize.  One workgroup of kFinalBlock threads; fixed-order reduction,
 // so the result depends only on the partials (bitwise reproducible for a given
-// launch shape).  `res_host` is host-mapped; the system-scope fence makes the
-// record visible to the host once the kernel has completed.
+// launch shape).  `res_host` is host-mapped and GPU-uncached; its sequence
+// number is stored last, with release semantics at system scope, so a host
+// that sees the expected sequence number sees the whole record.
 // ---------------------------------------------------------------------------
 constexpr int kFinalBlock = 256;
 
@@ -232,8 +233,12 @@ __global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restr
     if (threadIdx.x == 0) {
         const Result r = make_result(tot, loss_scale, clip, seq);
         *res = r;
-        *res_host = r;
-        __threadfence_system();
+        // publish to the host: the record first, then its sequence number with a
+        // system-scope release (the host polls the sequence number)
+        Result rh = r;
+        rh.seq = 0;
+        *res_host = rh;
+        __hip_atomic_store(&res_host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 

@@ -124,7 +124,7 @@ struct Ctx {
     zs::Result* res = nullptr;      // result record (device), read by the update kernel
     zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
     zs::Result* host_dev = nullptr; // its device-side address
-    hipEvent_t flag_ev = nullptr;   // recorded after the finalize kernel
+    hipEvent_t prof_last_end = nullptr;  // end event of the last profiled update on this stream
     uint32_t seq = 0;               // call counter echoed in the result record
     int ncu = 0;
     size_t stats_lds = 0, adam_lds = 0;
@@ -153,13 +153,11 @@ int get_ctx(hipStream_t stream, Ctx** out) {
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
-              hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess &&
-              hipEventCreateWithFlags(&c->flag_ev, hipEventDisableTiming) == hipSuccess;
+              hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess;
     if (!ok) {
         if (c->part) (void)hipFree(c->part);
         if (c->res) (void)hipFree(c->res);
         if (c->host) (void)hipHostFree(c->host);
-        if (c->flag_ev) (void)hipEventDestroy(c->flag_ev);
         (void)hipGetLastError();
         return fail(ZERO_ENOMEM, "could not allocate the step workspace on device %d", dev);
     }
@@ -170,10 +168,14 @@ int get_ctx(hipStream_t stream, Ctx** out) {
 }
 
 // ---------------------------------------------------------------------------
-// Profiling: events around the statistics and update kernels of each step.
+// Profiling: two events per step, before and after the update kernel.  The
+// statistics time of a step runs from the previous profiled update's end on
+// the same stream (or from an extra start event for the first one) to the
+// update's start.
 // ---------------------------------------------------------------------------
 struct ProfRec {
-    hipEvent_t e[3];  // before statistics, between the kernels, after the update
+    hipEvent_t start, mid, end;
+    bool own_start;  // start was recorded for this step (else it is the previous step's end)
 };
 
 std::mutex g_prof_mu;
@@ -194,19 +196,31 @@ hipEvent_t prof_event() {
     return e;
 }
 
+// Forget every stream's last end event (its handle is about to go back to the pool).
+void prof_forget_ends() {
+    std::lock_guard<std::mutex> lk(g_ctx_mu);
+    for (auto& kv : g_ctx)
+        kv.second->prof_last_end = nullptr;
+}
+
 int prof_drain_locked() {
     for (ProfRec& r : g_prof_pending) {
-        HIP_TRY(hipEventSynchronize(r.e[2]));
+        HIP_TRY(hipEventSynchronize(r.end));
         float a = 0.f, b = 0.f;
-        HIP_TRY(hipEventElapsedTime(&a, r.e[0], r.e[1]));
-        HIP_TRY(hipEventElapsedTime(&b, r.e[1], r.e[2]));
+        HIP_TRY(hipEventElapsedTime(&a, r.start, r.mid));
+        HIP_TRY(hipEventElapsedTime(&b, r.mid, r.end));
         g_prof_acc.steps += 1;
         g_prof_acc.stats_ms += a;
         g_prof_acc.update_ms += b;
-        for (hipEvent_t e : r.e)
-            g_prof_pool.push_back(e);
+    }
+    for (ProfRec& r : g_prof_pending) {
+        if (r.own_start)
+            g_prof_pool.push_back(r.start);
+        g_prof_pool.push_back(r.mid);
+        g_prof_pool.push_back(r.end);
     }
     g_prof_pending.clear();
+    prof_forget_ends();
     return 0;
 }
 
@@ -293,34 +307,55 @@ int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32,
     return ZERO_OK;
 }
 
-// Wait for the event recorded after the finalize kernel and read the mapped record.
-int read_result(Ctx* ctx, uint32_t seq, zs::Result* out) {
-    HIP_TRY(hipEventSynchronize(ctx->flag_ev));
+// Wait until the finalize kernel has published call `seq` in the host-mapped
+// record (it writes the record, then the sequence number with a system-scope
+// release), then read it.  No event is recorded on the stream for this: event
+// markers between kernels cost several microseconds of GPU idle time each.
+int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out) {
+    uint64_t polls = 0;
+    while (__atomic_load_n(&ctx->host->seq, __ATOMIC_ACQUIRE) != seq) {
+        __builtin_ia32_pause();
+        if ((++polls & 0xFFF) == 0) {
+            const hipError_t e = hipStreamQuery(stream);
+            if (e == hipSuccess) {  // everything queued has finished
+                if (__atomic_load_n(&ctx->host->seq, __ATOMIC_ACQUIRE) == seq)
+                    break;
+                return fail(ZERO_EHIP, "result record %u not published although the stream is idle", seq);
+            }
+            if (e != hipErrorNotReady)
+                return fail(ZERO_EHIP, "stream failed while waiting for the statistics: %s", hipGetErrorString(e));
+        }
+    }
     std::memcpy(out, (const void*)ctx->host, sizeof *out);
-    if (out->seq != seq)
-        return fail(ZERO_EHIP, "result record not published (seq %u, expected %u)", out->seq, seq);
     return ZERO_OK;
 }
 
 // Profiling events of one step (taken from a pool while profiling is on).
-bool prof_begin(ProfRec* pr) {
+// Returns false when profiling is off; rec->end == nullptr signals failure.
+bool prof_begin(Ctx* ctx, ProfRec* rec) {
     std::lock_guard<std::mutex> plk(g_prof_mu);
     if (!g_prof_on)
         return false;
-    for (hipEvent_t& e : pr->e)
-        e = prof_event();
-    if (!pr->e[0] || !pr->e[1] || !pr->e[2]) {
-        for (hipEvent_t e : pr->e)
-            if (e)
-                g_prof_pool.push_back(e);
-        pr->e[0] = nullptr;
+    rec->own_start = ctx->prof_last_end == nullptr;
+    rec->start = rec->own_start ? prof_event() : ctx->prof_last_end;
+    rec->mid = prof_event();
+    rec->end = prof_event();
+    if (!rec->start || !rec->mid || !rec->end) {
+        if (rec->own_start && rec->start)
+            g_prof_pool.push_back(rec->start);
+        if (rec->mid)
+            g_prof_pool.push_back(rec->mid);
+        if (rec->end)
+            g_prof_pool.push_back(rec->end);
+        rec->end = nullptr;
     }
     return true;
 }
 
-int prof_end(const ProfRec& pr) {
+int prof_end(Ctx* ctx, const ProfRec& rec) {
     std::lock_guard<std::mutex> plk(g_prof_mu);
-    g_prof_pending.push_back(pr);
+    g_prof_pending.push_back(rec);
+    ctx->prof_last_end = rec.end;
     if (g_prof_pending.size() >= 4096)
         return prof_drain_locked();
     return ZERO_OK;
@@ -429,26 +464,25 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     const uint32_t seq = ++ctx->seq;
 
     ProfRec pr{};
-    const bool prof = prof_begin(&pr);
-    if (prof && !pr.e[0])
+    const bool prof = prof_begin(ctx, &pr);
+    if (prof && !pr.end)
         return fail(ZERO_EHIP, "zero_shard_step: could not create a profiling event");
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[0], stream));
+    if (prof && pr.own_start)
+        HIP_TRY(hipEventRecord(pr.start, stream));
     if ((rc = launch_stats(ctx, grad16, n, pl, loss_scale, clip, seq, stream)))
         return rc;
-    HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
     if (prof)
-        HIP_TRY(hipEventRecord(pr.e[1], stream));
+        HIP_TRY(hipEventRecord(pr.mid, stream));
     if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
         return rc;
     if (prof) {
-        HIP_TRY(hipEventRecord(pr.e[2], stream));
-        if ((rc = prof_end(pr)))
+        HIP_TRY(hipEventRecord(pr.end, stream));
+        if ((rc = prof_end(ctx, pr)))
             return rc;
     }
     // The update kernel is already queued: wait only for the statistics and finalize kernels.
     zs::Result r;
-    if ((rc = read_result(ctx, seq, &r)))
+    if ((rc = wait_result(ctx, seq, stream, &r)))
         return rc;
     t_stats.sumsq = r.sumsq;
     t_stats.norm = r.norm;
@@ -483,9 +517,8 @@ int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, voi
     const uint32_t seq = ++ctx->seq;
     if ((rc = launch_stats(ctx, grad16, n, pl, 1.0, 0.0, seq, stream)))
         return rc;
-    HIP_TRY(hipEventRecord(ctx->flag_ev, stream));
     zs::Result r;
-    if ((rc = read_result(ctx, seq, &r)))
+    if ((rc = wait_result(ctx, seq, stream, &r)))
         return rc;
     *local_sumsq = r.sumsq;
     return ZERO_OK;
@@ -519,6 +552,7 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
 int zero_profile_enable(int32_t on) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     g_prof_on = on != 0;
+    prof_forget_ends();
     return ZERO_OK;
 }
 
