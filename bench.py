@@ -65,23 +65,26 @@ def measured_traffic(n):
 
 
 def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
-    """The oracle, as it stands, single-threaded on a bounded prefix of the shard."""
+    """The oracle, as it stands, single-threaded on the same shard, 4M-element chunk by chunk
+    (each chunk one oracle step: statistics + update), until about budget_s seconds of CPU
+    time have been spent (wrapping around the shard if it is done sooner)."""
     import numpy as np
     import oracle
     chunk = 1 << 22
-    done, t_used = 0, 0.0
+    done, t_used, pos = 0, 0.0, 0
     p16 = np.empty(min(n, chunk), np.uint16)
-    while done < n and t_used < budget_s:
-        b = min(n, done + chunk)
-        th, mm, vv = theta[done:b].copy(), m[done:b].copy(), v[done:b].copy()
+    while t_used < budget_s:
+        b = min(n, pos + chunk)
+        th, mm, vv = theta[pos:b].copy(), m[pos:b].copy(), v[pos:b].copy()
         t0 = time.perf_counter()
-        oracle.shard_step(g16[done:b], th, mm, vv, p16[:b - done], w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
+        oracle.shard_step(g16[pos:b], th, mm, vv, p16[:b - pos], w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
                           1, scale, w.clip)
         t_used += time.perf_counter() - t0
-        done = b
+        done += b - pos
+        pos = 0 if b == n else b
     return {"value": done / t_used, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": "first %d of %d shard elements, one step (stats + update), single thread, %.1f s"
-                      % (done, n, t_used)}
+            "sample": "%d element-updates of the %d-element shard in 4M-element oracle steps (statistics + "
+                      "update), single thread, %.1f s" % (done, n, t_used)}
 
 
 def main():
@@ -92,6 +95,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle CPU time")
+    ap.add_argument("--profile-every", type=int, default=10,
+                    help="time the kernels of one step in this many with HIP events (markers cost GPU time)")
     ap.add_argument("--probe-copy-mib", type=int, default=2048,
                     help="also run the library's copy kernel over this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -162,7 +167,7 @@ def main():
         step()
     torch.cuda.synchronize()
     zb.zero_profile_read()
-    zb.zero_profile_enable(True)
+    zb.zero_profile_enable(args.profile_every)
     skips = 0
     print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
     torch.cuda.synchronize()
@@ -202,7 +207,7 @@ def main():
                    "shard_numel": n, "parallelism": "one ZeRO P_os+g data-parallel rank (N_d=%d) per GPU" % w.nd},
         "hbm_gbps": step_gbps,
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
-        "kernel_ms": {"stats_and_finalize": stats_ms, "update": upd_ms},
+        "kernel_ms": {"stats_and_finalize": stats_ms, "update": upd_ms, "profiled_steps": prof.steps},
         "roofline": {"bound": "hbm", "kernel": "k_adam_vec", "achieved": upd_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},

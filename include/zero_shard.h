@@ -98,11 +98,13 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
  * caller then lowers its loss scale and does not advance t.
  *
  * All five arrays must be distinct, non-overlapping ranges; base pointers of
- * any element alignment are accepted (16-byte-aligned shards take the
- * vectorised path).  The call blocks until the skip decision is known (a few
- * bytes copied to pinned host memory); the update kernel may still be running
- * on `stream` when it returns.  Returns 0 applied, 1 skipped, ZERO_EINVAL /
- * ZERO_EHIP / ZERO_ENOMEM on error (on ZERO_EINVAL nothing is launched). */
+ * any element alignment are accepted (when all five share one misalignment
+ * the vectorised path runs after a few scalar head elements).  The call
+ * blocks until the skip decision is known (the statistics kernels publish it
+ * in host-mapped memory, which the calling thread polls); the update kernel
+ * may still be running on `stream` when it returns.  Returns 0 applied,
+ * 1 skipped, ZERO_EINVAL / ZERO_EHIP / ZERO_ENOMEM on error (on ZERO_EINVAL
+ * nothing is launched). */
 int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
                     int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
                     int64_t step, double loss_scale, double clip, void* stream);
@@ -195,18 +197,20 @@ int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, doubl
  * thread's next call into the library. */
 const char* zero_last_error(void);
 
-/* Kernel timing with HIP events on the call's own stream.  While enabled,
- * every zero_shard_step records events around its statistics kernels and its
- * update kernel.  zero_profile_read waits for the recorded work, then returns
- * the summed durations and the number of steps since enabling (or the last
- * read) and resets them. */
+/* Kernel timing with HIP events on the call's own stream.  With every = k > 0,
+ * one zero_shard_step in k on each stream records events before its
+ * statistics kernels, before its update kernel and after it (each event marker
+ * costs the GPU a few microseconds, hence the sampling); every = 0 disables.
+ * zero_profile_read waits for the recorded work, then returns the summed
+ * durations and the number of profiled steps since enabling (or the last read)
+ * and resets them.  ZERO_EINVAL for every < 0. */
 typedef struct {
     int64_t steps;      /* steps timed                                        */
     double stats_ms;    /* total time of the statistics + finalize kernels    */
     double update_ms;   /* total time of the fused update kernel              */
 } zero_profile_t;
 
-int zero_profile_enable(int32_t on);
+int zero_profile_enable(int32_t every);
 int zero_profile_read(zero_profile_t* out);
 
 /* Device-to-device copy of `bytes` bytes with the library's own streaming

@@ -192,8 +192,9 @@ def zero_last_error() -> str:
     return _lib.zero_last_error().decode(errors="replace")
 
 
-def zero_profile_enable(on: bool):
-    _check(_lib.zero_profile_enable(1 if on else 0))
+def zero_profile_enable(every):
+    """Profile one step in `every` (True = every step, False/0 = off)."""
+    _check(_lib.zero_profile_enable(int(every)))
 
 
 def zero_profile_read() -> Profile:

@@ -125,6 +125,7 @@ struct Ctx {
     zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
     zs::Result* host_dev = nullptr; // its device-side address
     hipEvent_t prof_last_end = nullptr;  // end event of the last profiled update on this stream
+    uint64_t prof_tick = 0;              // steps seen while profiling (for sampling)
     uint32_t seq = 0;               // call counter echoed in the result record
     int ncu = 0;
     size_t stats_lds = 0, adam_lds = 0;
@@ -179,7 +180,7 @@ struct ProfRec {
 };
 
 std::mutex g_prof_mu;
-bool g_prof_on = false;
+int32_t g_prof_every = 0;  // 0: off; k: profile one step in k on each stream
 std::vector<ProfRec> g_prof_pending;
 std::vector<hipEvent_t> g_prof_pool;
 zero_profile_t g_prof_acc = {0, 0.0, 0.0};
@@ -334,8 +335,12 @@ int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out) {
 // Returns false when profiling is off; rec->end == nullptr signals failure.
 bool prof_begin(Ctx* ctx, ProfRec* rec) {
     std::lock_guard<std::mutex> plk(g_prof_mu);
-    if (!g_prof_on)
+    if (g_prof_every <= 0)
         return false;
+    if (ctx->prof_tick++ % (uint64_t)g_prof_every != 0) {
+        ctx->prof_last_end = nullptr;  // the chain of back-to-back profiled steps is broken
+        return false;
+    }
     rec->own_start = ctx->prof_last_end == nullptr;
     rec->start = rec->own_start ? prof_event() : ctx->prof_last_end;
     rec->mid = prof_event();
@@ -549,10 +554,15 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     return launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
 }
 
-int zero_profile_enable(int32_t on) {
+int zero_profile_enable(int32_t every) {
+    if (every < 0)
+        return fail(ZERO_EINVAL, "zero_profile_enable: every must be >= 0");
     std::lock_guard<std::mutex> lk(g_prof_mu);
-    g_prof_on = on != 0;
+    g_prof_every = every;
     prof_forget_ends();
+    std::lock_guard<std::mutex> lk2(g_ctx_mu);
+    for (auto& kv : g_ctx)
+        kv.second->prof_tick = 0;
     return ZERO_OK;
 }
 

@@ -165,3 +165,8 @@ def test_stats_rejects_invalid_arguments(zb):
     assert lib.zero_shard_stats(GOOD[0], -3, ctypes.byref(out), None) == zb.ZERO_EINVAL
     assert lib.zero_shard_stats(GOOD[0], 10, None, None) == zb.ZERO_EINVAL
     assert lib.zero_shard_stats(None, 0, ctypes.byref(out), None) == zb.ZERO_OK and out.value == 0.0
+
+
+def test_profile_enable_rejects_negative(zb):
+    assert zb.raw_library().zero_profile_enable(-1) == zb.ZERO_EINVAL
+    assert zb.raw_library().zero_profile_enable(0) == zb.ZERO_OK

@@ -287,3 +287,20 @@ def test_profile_counts_steps(env):
     zb.zero_profile_enable(False)
     p = zb.zero_profile_read()
     assert p.steps == 3 and p.stats_ms > 0 and p.update_ms > 0
+
+
+def test_profile_samples_one_step_in_k(env):
+    torch, zb, dev = env
+    n = 1 << 20
+    g16, theta, m, v = workloads.random_case(8, n)
+    bufs = _alloc(torch, dev, n)
+    for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    zb.zero_profile_read()
+    zb.zero_profile_enable(3)
+    for t in range(1, 8):
+        zb.zero_shard_step(bufs[0].view, bufs[1].view, bufs[2].view, bufs[3].view, bufs[4].view,
+                           1e-4, 0.9, 0.999, 1e-8, 0.0, t, 2.0 ** 16, 1.0)
+    zb.zero_profile_enable(0)
+    p = zb.zero_profile_read()
+    assert p.steps == 3 and p.update_ms > 0  # steps 1, 4 and 7
