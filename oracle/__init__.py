@@ -56,6 +56,8 @@ def lib():
             L.zo_f16_to_f32.restype = flt
             L.zo_f32_to_f16.argtypes = [flt]
             L.zo_f32_to_f16.restype = ctypes.c_uint16
+            L.zo_f32_to_f16_array.argtypes = [P, P, i64]
+            L.zo_f32_to_f16_array.restype = None
             L.zo_local_stats.argtypes = [P, i64, P, P]
             L.zo_local_stats.restype = None
             L.zo_u128_to_double.argtypes = [P]
@@ -107,6 +109,14 @@ def f16_to_f32(h: int) -> float:
 
 def f32_to_f16(x: float) -> int:
     return int(lib().zo_f32_to_f16(x))
+
+
+def f32_to_f16_array(x: np.ndarray) -> np.ndarray:
+    """Element-wise binary16 encoding (uint16 bit patterns) of a float32 array."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.size, np.uint16)
+    lib().zo_f32_to_f16_array(_ptr(x, np.float32), _ptr(out, np.uint16), x.size)
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -15,6 +15,7 @@
  *                     (S = ceil(Psi/N_d), shard r = [r*S, r*S+S)).
  *   zo_f16_to_f32     IEEE 754 binary16 decoding (the fp16 gradients and
  *   zo_f32_to_f16     parameters of Sec. 3.1's mixed-precision training),
+ *   zo_f32_to_f16_array
  *                     written from the format definition; encoding rounds to
  *                     nearest, ties to even.
  *   zo_local_stats    Sec. 3.2 names the gradient-norm computation over the
@@ -137,6 +138,13 @@ uint16_t zo_f32_to_f16(float x)
     if (E > 15)
         return (uint16_t)(sign | 0x7C00u);
     return (uint16_t)(sign | (uint16_t)((E + 15) << 10) | (uint16_t)(k - 1024.0));
+}
+
+/* Element-wise zo_f32_to_f16 over an array (for exhaustive checks). */
+void zo_f32_to_f16_array(const float* x, uint16_t* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = zo_f32_to_f16(x[i]);
 }
 
 /* ------------------------------------------------------------------------ */

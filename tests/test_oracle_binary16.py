@@ -1,6 +1,8 @@
 """Pins of the oracle's binary16 coding (the fp16 gradients and parameters of
 mixed-precision training, ZeRO Sec. 3.1) against numpy's float16 conversions,
 an independent library implementation of IEEE 754 binary16."""
+import os
+
 import numpy as np
 
 import oracle
@@ -54,3 +56,26 @@ def test_encode_special_values():
                    2.0 ** -24, 3 * 2.0 ** -26, 2.0 ** -14, 2.0 ** -14 - 2.0 ** -25], np.float32)
     _check_encode(xs)
     assert oracle.f32_to_f16(float("nan")) & 0x7C00 == 0x7C00
+
+
+def test_encode_exhaustive_over_all_fp32_patterns():
+    # Every one of the 2^32 fp32 bit patterns, in parallel chunks; NaNs must stay NaN.
+    from concurrent.futures import ThreadPoolExecutor
+    chunk = 1 << 26
+
+    def check(c):
+        bits = np.arange(c * chunk, (c + 1) * chunk, dtype=np.uint64).astype(np.uint32)
+        x = bits.view(np.float32)
+        got = oracle.f32_to_f16_array(x)
+        with np.errstate(over="ignore"):
+            ref = x.astype(np.float16).view(np.uint16)
+        nan = np.isnan(x)
+        bad = np.flatnonzero((got != ref) & ~nan)
+        nan_ok = bool(np.all((got[nan] & 0x7C00) == 0x7C00) and np.all((got[nan] & 0x3FF) != 0))
+        return bad.size, (int(bits[bad[0]]) if bad.size else None), nan_ok
+
+    workers = max(1, min(8, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        results = list(ex.map(check, range((1 << 32) // chunk)))
+    assert sum(r[0] for r in results) == 0, [hex(r[1]) for r in results if r[1] is not None][:5]
+    assert all(r[2] for r in results)

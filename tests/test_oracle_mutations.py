@@ -63,7 +63,8 @@ def _build_mutant(tmp, name, old, new):
 
 def _suite_fails(lib):
     env = dict(os.environ, ZERO_ORACLE_LIB=lib)
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PIN_TESTS],
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-k", "not exhaustive",
+                        *PIN_TESTS],
                        cwd=ROOT, env=env, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, timeout=600)
     return r.returncode != 0, r.stdout.decode(errors="replace")[-400:]
 
