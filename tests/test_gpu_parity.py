@@ -304,3 +304,32 @@ def test_profile_samples_one_step_in_k(env):
     zb.zero_profile_enable(0)
     p = zb.zero_profile_read()
     assert p.steps == 3 and p.update_ms > 0  # steps 1, 4 and 7
+
+
+def test_checkpoint_resume_equals_straight_run(env, tmp_path):
+    # The state is exactly master/m/v (+ the scaler's t and scale): saving it after 5 steps
+    # and resuming in fresh buffers gives the same bytes as 10 uninterrupted steps.
+    torch, zb, dev = env
+    n = 500_003
+    grads = [workloads.random_case(300 + k, n)[0] for k in range(10)]
+    _, theta, m, v = workloads.random_case(299, n)
+
+    def run(state, ks, t0):
+        bufs = _alloc(torch, dev, n)
+        for b, a in zip(bufs[1:4], state):
+            b.upload(a)
+        bufs[4].upload(workloads.p16_sentinel(n))
+        for k in ks:
+            bufs[0].upload(grads[k])
+            assert zb.zero_shard_step(*(b.view for b in bufs), 1e-4, 0.9, 0.999, 1e-8, 0.0, t0 + k, 2.0 ** 16,
+                                      1.0) == 0
+        torch.cuda.synchronize()
+        return [b.download().copy() for b in bufs[1:]]
+
+    straight = run((theta, m, v), range(10), 1)
+    first = run((theta, m, v), range(5), 1)
+    np.savez(tmp_path / "ckpt.npz", master=first[0], m=first[1], v=first[2])
+    ck = np.load(tmp_path / "ckpt.npz")
+    resumed = run((ck["master"], ck["m"], ck["v"]), range(5, 10), 1)
+    for a, b in zip(straight, resumed):
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
