@@ -17,6 +17,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,16 +33,25 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_adam_vec_mp16_dp25_100b_traffic
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1910_02054_amd", "csrc", f) for f in ("shard_kernels.hpp", "zero_shard.hip")]
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and blank lines (what the compiler sees of it)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.strip() for line in text.splitlines() if line.strip())
+
+
 def kernel_source_hash() -> str:
-    """Hash of the kernels' source and of the production launch policy (the block of
-    zero_shard.hip that fixes block sizes, unrolls, cache policies and occupancy caps)."""
+    """Hash of the kernels' code and of the production launch policy (the constexpr block of
+    zero_shard.hip that fixes block sizes, unrolls, cache policies and occupancy caps);
+    comments and layout do not count."""
     h = hashlib.sha256()
-    with open(KERNEL_SOURCES[0], "rb") as f:
-        h.update(f.read())
+    with open(KERNEL_SOURCES[0]) as f:
+        h.update(_code_only(f.read()).encode())
     with open(KERNEL_SOURCES[1]) as f:
         host = f.read()
-    a, b = host.index("// Production launch policy"), host.index("struct Plan {")
-    h.update(host[a:b].encode())
+    a, b = host.index("constexpr int kStatsBlock"), host.index("struct Plan {")
+    policy = [ln for ln in _code_only(host[a:b]).splitlines() if ln.startswith("constexpr")]
+    h.update("\n".join(policy).encode())
     return h.hexdigest()[:16]
 
 

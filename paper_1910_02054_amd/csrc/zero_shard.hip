@@ -47,9 +47,6 @@ int fail(int code, const char* fmt, ...) {
     } while (0)
 
 // ---------------------------------------------------------------------------
-// Launch planning.  One function decides every launch shape from n, so tests
-// and benchmarks exercise the same configuration.
-// ---------------------------------------------------------------------------
 // Production launch policy of the streaming kernels (template knobs in
 // shard_kernels.hpp), chosen by measurement on MI355X in the two-kernel step
 // flow.  The HBM efficiency of these streams peaks well below full occupancy,
@@ -57,6 +54,7 @@ int fail(int code, const char* fmt, ...) {
 // workgroup) are launched with an LDS reservation that caps resident
 // workgroups per CU.  The statistics pass uses cache-allocating loads, which
 // leaves part of the gradient in the Infinity Cache for the update.
+// ---------------------------------------------------------------------------
 constexpr int kStatsBlock = 64, kStatsUnroll = 4, kStatsPerCU = 8;
 constexpr bool kStatsNTL = false, kStatsXCD = false;
 constexpr int kAdamBlock = 64, kAdamUnroll = 1, kAdamPerCU = 12;
@@ -65,6 +63,10 @@ constexpr int64_t kAdamMaxBlocks = 1 << 26;
 constexpr int kCopyBlock = 64, kCopyUnroll = 1;
 constexpr bool kCopyNTL = true, kCopyNTS = true, kCopyXCD = false;
 
+// ---------------------------------------------------------------------------
+// Launch planning.  One function decides every launch shape from n and the
+// arrays' alignments, so tests and benchmarks exercise the same configuration.
+// ---------------------------------------------------------------------------
 struct Plan {
     int64_t ghead, gvec;   // statistics: unaligned head elements, 8-element vectors
     int stats_blocks;
@@ -107,12 +109,36 @@ Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* 
     return pl;
 }
 
-// Dynamic LDS that caps resident workgroups of a kernel at `per_cu` per CU
-// (a workgroup's LDS is its static LDS plus this reservation).
-size_t occupancy_lds(size_t lds_per_cu, size_t lds_per_block, int per_cu) {
-    size_t l = (lds_per_cu / (size_t)per_cu) & ~(size_t)511;
-    const size_t cap = lds_per_block > 1024 ? lds_per_block - 1024 : 0;  // room for static LDS
-    return l > cap ? cap : l;
+// Dynamic LDS that caps the resident workgroups of `kernel` (launched with
+// `block` threads) at `per_cu` per CU: an equal share of the CU's LDS minus the
+// kernel's own static LDS, lowered granule by granule until the runtime's
+// occupancy calculator admits `per_cu` workgroups.  *resident receives what
+// the calculator reports for the returned reservation.
+size_t occupancy_lds(const void* kernel, int block, int per_cu, const hipDeviceProp_t& prop, int* resident) {
+    const size_t granule = 512;
+    *resident = 0;
+    hipFuncAttributes attr;
+    if (hipFuncGetAttributes(&attr, kernel) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    const size_t fixed = (attr.sharedSizeBytes + granule - 1) & ~(granule - 1);
+    const size_t share = ((size_t)prop.maxSharedMemoryPerMultiProcessor / (size_t)per_cu) & ~(granule - 1);
+    const size_t cap = (size_t)prop.sharedMemPerBlock > fixed + granule ? prop.sharedMemPerBlock - fixed - granule : 0;
+    size_t r = share > fixed ? share - fixed : 0;
+    if (r > cap)
+        r = cap;
+    for (;;) {
+        int blocks = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, block, r) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        *resident = blocks;
+        if (blocks >= per_cu || r < granule)
+            return r;
+        r -= granule;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -128,7 +154,8 @@ struct Ctx {
     uint64_t prof_tick = 0;              // steps seen while profiling (for sampling)
     uint32_t seq = 0;               // call counter echoed in the result record
     int ncu = 0;
-    size_t stats_lds = 0, adam_lds = 0;
+    size_t stats_lds = 0, adam_lds = 0;   // occupancy reservations (dynamic LDS per workgroup)
+    int stats_resident = 0, adam_resident = 0;
 };
 
 std::mutex g_ctx_mu;
@@ -148,8 +175,12 @@ int get_ctx(hipStream_t stream, Ctx** out) {
     HIP_TRY(hipGetDeviceProperties(&prop, dev));
     std::unique_ptr<Ctx> c(new Ctx);
     c->ncu = prop.multiProcessorCount;
-    c->stats_lds = occupancy_lds(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock, kStatsPerCU);
-    c->adam_lds = occupancy_lds(prop.maxSharedMemoryPerMultiProcessor, prop.sharedMemPerBlock, kAdamPerCU);
+    c->stats_lds = occupancy_lds(
+        reinterpret_cast<const void*>(zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>), kStatsBlock,
+        kStatsPerCU, prop, &c->stats_resident);
+    c->adam_lds = occupancy_lds(
+        reinterpret_cast<const void*>(zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>),
+        kAdamBlock, kAdamPerCU, prop, &c->adam_resident);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
@@ -230,6 +261,14 @@ bool is_fin(double x) { return std::isfinite(x); }
 bool overlaps(uintptr_t a, size_t an, uintptr_t b, size_t bn) { return a < b + bn && b < a + an; }
 
 constexpr int64_t kMaxNumel = (int64_t)1 << 40;
+
+// Call sequence numbers skip 0: the finalize kernel writes the host record with
+// sequence number 0 before publishing the real one.
+uint32_t next_seq(Ctx* ctx) {
+    if (++ctx->seq == 0)
+        ++ctx->seq;
+    return ctx->seq;
+}
 
 // Argument checks shared by zero_shard_step and zero_shard_apply; nothing is
 // launched unless every check passes.
@@ -466,7 +505,7 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     std::lock_guard<std::mutex> lk(ctx->mu);
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
-    const uint32_t seq = ++ctx->seq;
+    const uint32_t seq = next_seq(ctx);
 
     ProfRec pr{};
     const bool prof = prof_begin(ctx, &pr);
@@ -519,7 +558,7 @@ int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, voi
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
     const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
-    const uint32_t seq = ++ctx->seq;
+    const uint32_t seq = next_seq(ctx);
     if ((rc = launch_stats(ctx, grad16, n, pl, 1.0, 0.0, seq, stream)))
         return rc;
     zs::Result r;
@@ -548,7 +587,7 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     std::lock_guard<std::mutex> lk(ctx->mu);
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
-    const uint32_t seq = ++ctx->seq;
+    const uint32_t seq = next_seq(ctx);
     zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
     HIP_TRY(hipGetLastError());
     return launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
