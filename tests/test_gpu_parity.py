@@ -333,3 +333,48 @@ def test_checkpoint_resume_equals_straight_run(env, tmp_path):
     resumed = run((ck["master"], ck["m"], ck["v"]), range(5, 10), 1)
     for a, b in zip(straight, resumed):
         assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+
+
+@pytest.mark.parametrize("same_stream", [False, True])
+def test_concurrent_host_threads(env, same_stream):
+    # Calls overlap in the library (ctypes releases the GIL): each stream has its own workspace,
+    # and calls that share a stream are serialised.  Every thread's result must match the oracle.
+    import threading
+    torch, zb, dev = env
+    n = 400_009
+    shared = torch.cuda.Stream()
+    cases = []
+    for k in range(3):
+        g16, theta, m, v = workloads.random_case(400 + k, n)
+        bufs = _alloc(torch, dev, n)
+        for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+            b.upload(a)
+        cases.append((bufs, [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)], g16))
+    torch.cuda.synchronize()
+    errors = []
+
+    def work(k):
+        try:
+            bufs, _, _ = cases[k]
+            s = shared if same_stream else torch.cuda.Stream()
+            for t in range(1, 4):
+                f = zb.zero_shard_step(*(b.view for b in bufs), 1e-4, 0.9, 0.999, 1e-8, 0.0, t, 2.0 ** 16, 1.0,
+                                       stream=s)
+                assert f == 0
+            s.synchronize()
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(3)]
+    say("concurrent threads, same stream:", same_stream)
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for bufs, ref, g16 in cases:
+        for t in range(1, 4):
+            H.oracle_step(g16, *ref, 1e-4, 0.9, 0.999, 1e-8, 0.0, t, 2.0 ** 16, 1.0)
+        H.compare_state([b.download() for b in bufs[1:]], ref)
+        assert all(b.guards_intact() for b in bufs)

@@ -114,3 +114,13 @@ def test_bad_arguments():
         oracle.model_state_bytes(1e9, 0, oracle.STAGE_OS)
     with pytest.raises(ValueError):
         oracle.model_state_bytes(1e9, 4, 7)
+
+
+def test_4psi_plus_12psi_over_nd_is_the_pos_stage():
+    # 2*Psi + 2*Psi + 12*Psi/N_d is the P_os memory (Sec. 5.1: 31.4 GB at 7.5B, N_d = 64);
+    # P_os+g is 2*Psi + 14*Psi/N_d (Sec. 5.2: 16.6 GB).  Only P_os matches the first form.
+    psi, nd = 7.5e9, 64
+    form = 2 * psi + 2 * psi + 12 * psi / nd
+    assert oracle.model_state_bytes(psi, nd, oracle.STAGE_OS) == pytest.approx(form, rel=1e-15)
+    assert oracle.model_state_bytes(psi, nd, oracle.STAGE_OS_G) / 1e9 == pytest.approx(16.640625)
+    assert oracle.model_state_bytes(psi, nd, oracle.STAGE_OS_G) != pytest.approx(form, rel=1e-3)
