@@ -22,7 +22,8 @@
  *     first use and held until the process ends.  Its size does not depend on
  *     n (constant-size buffers, Sec. 6.2).
  *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.  The
- *     device is the current HIP device of the calling thread.
+ *     device is the current HIP device of the calling thread; a stream of
+ *     another device is rejected with ZERO_EINVAL.
  *   - Concurrent calls are serialised per (device, stream) by the library.
  */
 #ifndef ZERO_SHARD_H
@@ -138,6 +139,21 @@ int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, voi
 int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
                      int64_t n, double global_sumsq, double lr, double beta1, double beta2, double eps,
                      double weight_decay, int64_t step, double loss_scale, double clip, void* stream);
+
+/* The array checks of zero_shard_step without launching anything: n range,
+ * NULL pointers, alignment, that each array [p, p + n*size) lies inside one
+ * GPU-accessible allocation (hipMemGetAddressRange), then overlap.
+ * zero_shard_step, zero_shard_apply and zero_shard_stats make the same
+ * allocation check, so an n that overruns its allocation or a pageable host
+ * pointer is rejected with ZERO_EINVAL rather than faulting the GPU.  Limits:
+ * the allocation is what the HIP runtime handed out, so a caching allocator's
+ * segment (larger than the tensor carved from it) bounds the check; and step
+ * and apply remember the last (arrays, n) that passed on each stream and skip
+ * the lookup while they repeat, so a buffer freed and re-allocated smaller at
+ * the same address is caught only by calling this function.
+ * Returns 0 or ZERO_EINVAL. */
+int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
+                        const uint16_t* param16_out, int64_t n);
 
 /* Statistics of the calling thread's last successful zero_shard_step. */
 typedef struct {

@@ -50,6 +50,7 @@ _lib.zero_partition_layout.argtypes = [_i64, _i32, _i32, ctypes.POINTER(Layout)]
 _lib.zero_shard_step.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
 _lib.zero_shard_stats.argtypes = [_P, _i64, ctypes.POINTER(_dbl), _P]
 _lib.zero_shard_apply.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
+_lib.zero_shard_validate.argtypes = [_P, _P, _P, _P, _P, _i64]
 _lib.zero_shard_last_stats.argtypes = [ctypes.POINTER(StepStats)]
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
@@ -60,13 +61,13 @@ _lib.zero_profile_enable.argtypes = [_i32]
 _lib.zero_profile_read.argtypes = [ctypes.POINTER(Profile)]
 _lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
 for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
-           "zero_shard_last_stats", "zero_scaler_init",
+           "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
            "zero_probe_copy"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
-           "zero_shard_last_stats", "zero_scaler_init",
+           "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
            "zero_profile_read", "zero_probe_copy")
 
@@ -155,6 +156,12 @@ def zero_shard_apply(grad16, master32, m32, v32, param16_out, global_sumsq, lr, 
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(global_sumsq), float(lr),
         float(beta1), float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
         _stream(stream)))
+
+
+def zero_shard_validate(grad16, master32, m32, v32, param16_out, n):
+    """zero_shard_step's array checks without launching anything; raises ZeroError."""
+    return _check(_lib.zero_shard_validate(_addr(grad16), _addr(master32), _addr(m32), _addr(v32),
+                                           _addr(param16_out), int(n)))
 
 
 def zero_shard_last_stats() -> StepStats:

@@ -156,6 +156,7 @@ struct Ctx {
     int ncu = 0;
     size_t stats_lds = 0, adam_lds = 0;   // occupancy reservations (dynamic LDS per workgroup)
     int stats_resident = 0, adam_resident = 0;
+    uintptr_t checked[6] = {0, 0, 0, 0, 0, 0};  // last (arrays, n) whose ranges were verified
 };
 
 std::mutex g_ctx_mu;
@@ -164,6 +165,12 @@ std::map<std::pair<int, hipStream_t>, std::unique_ptr<Ctx>> g_ctx;
 int get_ctx(hipStream_t stream, Ctx** out) {
     int dev = 0;
     HIP_TRY(hipGetDevice(&dev));
+    if (stream) {
+        hipDevice_t sdev = 0;
+        HIP_TRY(hipStreamGetDevice(stream, &sdev));
+        if ((int)sdev != dev)
+            return fail(ZERO_EINVAL, "stream belongs to device %d but the current device is %d", (int)sdev, dev);
+    }
     std::lock_guard<std::mutex> lk(g_ctx_mu);
     auto key = std::make_pair(dev, stream);
     auto it = g_ctx.find(key);
@@ -272,11 +279,52 @@ uint32_t next_seq(Ctx* ctx) {
 
 // Argument checks shared by zero_shard_step and zero_shard_apply; nothing is
 // launched unless every check passes.
+constexpr size_t kElemSize[5] = {2, 4, 4, 4, 2};  // grad16, master32, m32, v32, param16_out
+
+int check_arrays_basic(const char* fn, const uintptr_t a[5], int64_t n) {
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "%s: n=%lld outside [0, 2^40]", fn, (long long)n);
+    if (n > 0) {
+        for (int i = 0; i < 5; ++i)
+            if (!a[i])
+                return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
+        for (int i = 0; i < 5; ++i)
+            if (a[i] % kElemSize[i])
+                return fail(ZERO_EINVAL, "%s: array %d is not %zu-byte aligned", fn, i, kElemSize[i]);
+    }
+    return ZERO_OK;
+}
+
+int check_arrays_disjoint(const char* fn, const uintptr_t a[5], int64_t n) {
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (overlaps(a[i], kElemSize[i] * (size_t)n, a[j], kElemSize[j] * (size_t)n))
+                return fail(ZERO_EINVAL, "%s: arrays %d and %d overlap", fn, i, j);
+    return ZERO_OK;
+}
+
+void array_addrs(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
+                 const uint16_t* param16_out, uintptr_t a[5]) {
+    a[0] = reinterpret_cast<uintptr_t>(grad16);
+    a[1] = reinterpret_cast<uintptr_t>(master32);
+    a[2] = reinterpret_cast<uintptr_t>(m32);
+    a[3] = reinterpret_cast<uintptr_t>(v32);
+    a[4] = reinterpret_cast<uintptr_t>(param16_out);
+}
+
+int check_arrays(const char* fn, const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
+                 const uint16_t* param16_out, int64_t n) {
+    uintptr_t a[5];
+    array_addrs(grad16, master32, m32, v32, param16_out, a);
+    int rc = check_arrays_basic(fn, a, n);
+    if (rc || n == 0)
+        return rc;
+    return check_arrays_disjoint(fn, a, n);
+}
+
 int check_update_args(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
                       const float* v32, const uint16_t* param16_out, int64_t n, double lr, double beta1,
                       double beta2, double eps, double weight_decay, int64_t step, double loss_scale, double clip) {
-    if (n < 0 || n > kMaxNumel)
-        return fail(ZERO_EINVAL, "%s: n=%lld outside [0, 2^40]", fn, (long long)n);
     if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
         return fail(ZERO_EINVAL, "%s: need finite lr >= 0, eps >= 0, weight_decay", fn);
     if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
@@ -287,22 +335,51 @@ int check_update_args(const char* fn, const uint16_t* grad16, const float* maste
         return fail(ZERO_EINVAL, "%s: loss_scale must be finite and > 0", fn);
     if (std::isnan(clip))
         return fail(ZERO_EINVAL, "%s: clip is NaN", fn);
-    if (n > 0) {
-        if (!grad16 || !master32 || !m32 || !v32 || !param16_out)
-            return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
-        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
-                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
-                                reinterpret_cast<uintptr_t>(param16_out)};
-        const size_t sz[5] = {2, 4, 4, 4, 2};
-        for (int i = 0; i < 5; ++i)
-            if (a[i] % sz[i])
-                return fail(ZERO_EINVAL, "%s: array %d is not %zu-byte aligned", fn, i, sz[i]);
-        for (int i = 0; i < 5; ++i)
-            for (int j = i + 1; j < 5; ++j)
-                if (overlaps(a[i], sz[i] * (size_t)n, a[j], sz[j] * (size_t)n))
-                    return fail(ZERO_EINVAL, "%s: arrays %d and %d overlap", fn, i, j);
+    return check_arrays(fn, grad16, master32, m32, v32, param16_out, n);
+}
+
+// Every array must lie inside one allocation the GPU can access: [p, p + bytes)
+// within the range hipMemGetAddressRange reports for p.  This turns an n that
+// overruns a buffer, or a pageable host pointer, into ZERO_EINVAL instead of a
+// GPU memory fault.
+int check_ranges(const char* fn, const void* const* ptrs, const size_t* bytes, int count) {
+    for (int i = 0; i < count; ++i) {
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        if (hipMemGetAddressRange(&base, &size, const_cast<void*>(ptrs[i])) != hipSuccess || !base) {
+            (void)hipGetLastError();
+            return fail(ZERO_EINVAL, "%s: array %d is not in GPU-accessible memory", fn, i);
+        }
+        const uintptr_t b = reinterpret_cast<uintptr_t>(base), p = reinterpret_cast<uintptr_t>(ptrs[i]);
+        if (p < b || p - b + bytes[i] > size)
+            return fail(ZERO_EINVAL, "%s: array %d ([%p, +%zu B)) overruns its allocation ([%p, +%zu B))", fn, i,
+                        ptrs[i], bytes[i], base, size);
     }
     return ZERO_OK;
+}
+
+int check_shard_ranges(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
+                       const float* v32, const uint16_t* param16_out, int64_t n) {
+    const void* ptrs[5] = {grad16, master32, m32, v32, param16_out};
+    size_t bytes[5];
+    for (int i = 0; i < 5; ++i)
+        bytes[i] = kElemSize[i] * (size_t)n;
+    return check_ranges(fn, ptrs, bytes, 5);
+}
+
+// The range check once per distinct (arrays, n) on a stream: a training loop
+// that reuses its buffers pays for it once.
+int check_shard_ranges_cached(Ctx* ctx, const char* fn, const uint16_t* grad16, const float* master32,
+                              const float* m32, const float* v32, const uint16_t* param16_out, int64_t n) {
+    const uintptr_t key[6] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
+                              reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
+                              reinterpret_cast<uintptr_t>(param16_out), (uintptr_t)n};
+    if (std::memcmp(key, ctx->checked, sizeof key) == 0)
+        return ZERO_OK;
+    const int rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n);
+    if (rc == ZERO_OK)
+        std::memcpy(ctx->checked, key, sizeof key);
+    return rc;
 }
 
 // fp32 constants, each computed in double and rounded once (the bias
@@ -503,6 +580,8 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     if ((rc = get_ctx(stream, &ctx)))
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
+    if ((rc = check_shard_ranges_cached(ctx, "zero_shard_step", grad16, master32, m32, v32, param16_out, n)))
+        return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
     const uint32_t seq = next_seq(ctx);
@@ -557,6 +636,12 @@ int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, voi
     if (rc)
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
+    {
+        const void* ptr = grad16;
+        const size_t bytes = 2 * (size_t)n;
+        if ((rc = check_ranges("zero_shard_stats", &ptr, &bytes, 1)))
+            return rc;
+    }
     const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
     const uint32_t seq = next_seq(ctx);
     if ((rc = launch_stats(ctx, grad16, n, pl, 1.0, 0.0, seq, stream)))
@@ -585,12 +670,28 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     if ((rc = get_ctx(stream, &ctx)))
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
+    if ((rc = check_shard_ranges_cached(ctx, "zero_shard_apply", grad16, master32, m32, v32, param16_out, n)))
+        return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
     const uint32_t seq = next_seq(ctx);
     zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
     HIP_TRY(hipGetLastError());
     return launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
+}
+
+int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
+                        const uint16_t* param16_out, int64_t n) {
+    // The allocation check comes before the disjointness check here, so an n that
+    // overruns the buffers is reported as such.
+    uintptr_t a[5];
+    array_addrs(grad16, master32, m32, v32, param16_out, a);
+    int rc = check_arrays_basic("zero_shard_validate", a, n);
+    if (rc || n == 0)
+        return rc;
+    if ((rc = check_shard_ranges("zero_shard_validate", grad16, master32, m32, v32, param16_out, n)))
+        return rc;
+    return check_arrays_disjoint("zero_shard_validate", a, n);
 }
 
 int zero_profile_enable(int32_t every) {

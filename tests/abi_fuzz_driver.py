@@ -54,4 +54,9 @@ for _ in range(5000):
 L.zero_shard_stats(None, 10, ctypes.byref(out), None)
 L.zero_shard_stats(None, 0, ctypes.byref(out), None)
 L.zero_profile_enable(-1); L.zero_profile_enable(0)
+L.zero_shard_validate.argtypes = [P, P, P, P, P, i64]
+for _ in range(2000):
+    ptrs = [p + r.choice([0, 1, 2, 8]) for p in G]
+    L.zero_shard_validate(*ptrs, r.choice([-1, 0, 10, 1 << 41]))
+    L.zero_last_error()
 print("driver done", bad, "rejected or empty calls")

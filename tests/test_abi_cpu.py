@@ -170,3 +170,16 @@ def test_stats_rejects_invalid_arguments(zb):
 def test_profile_enable_rejects_negative(zb):
     assert zb.raw_library().zero_profile_enable(-1) == zb.ZERO_EINVAL
     assert zb.raw_library().zero_profile_enable(0) == zb.ZERO_OK
+
+
+def test_validate_rejects_without_launching(zb):
+    lib = zb.raw_library()
+    lib.zero_shard_validate.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int64]
+    assert lib.zero_shard_validate(*GOOD, -1) == zb.ZERO_EINVAL
+    assert lib.zero_shard_validate(GOOD[0] + 1, *GOOD[1:], 10) == zb.ZERO_EINVAL
+    assert lib.zero_shard_validate(GOOD[0], GOOD[1], GOOD[1] + 8, *GOOD[3:], 10) == zb.ZERO_EINVAL  # no GPU memory
+    assert lib.zero_shard_validate(0, *GOOD[1:], 10) == zb.ZERO_EINVAL
+    assert lib.zero_shard_validate(0, 0, 0, 0, 0, 0) == zb.ZERO_OK
+    # plausible addresses that are not GPU allocations (no GPU here at all): rejected
+    assert lib.zero_shard_validate(*GOOD, 10) == zb.ZERO_EINVAL
+    assert "GPU-accessible" in zb.zero_last_error()

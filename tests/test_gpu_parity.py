@@ -378,3 +378,20 @@ def test_concurrent_host_threads(env, same_stream):
             H.oracle_step(g16, *ref, 1e-4, 0.9, 0.999, 1e-8, 0.0, t, 2.0 ** 16, 1.0)
         H.compare_state([b.download() for b in bufs[1:]], ref)
         assert all(b.guards_intact() for b in bufs)
+
+
+def test_validate_catches_overruns_and_host_memory(env):
+    # Only zero_shard_validate is called with bad arguments: nothing is ever launched on them.
+    torch, zb, dev = env
+    n = 1000
+    bufs = _alloc(torch, dev, n)
+    views = [b.view for b in bufs]
+    assert zb.zero_shard_validate(*views, n) == 0
+    with pytest.raises(zb.ZeroError) as e:
+        zb.zero_shard_validate(*views, 10 ** 9)
+    assert e.value.code == zb.ZERO_EINVAL and "overruns" in str(e.value)
+    host = [np.zeros(n, np.uint16), np.zeros(n, np.float32), np.zeros(n, np.float32), np.zeros(n, np.float32),
+            np.zeros(n, np.uint16)]
+    with pytest.raises(zb.ZeroError) as e:
+        zb.zero_shard_validate(*(h.ctypes.data for h in host), n)
+    assert e.value.code == zb.ZERO_EINVAL
