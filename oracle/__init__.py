@@ -76,6 +76,13 @@ def lib():
             L.zo_scaler_update.argtypes = [ctypes.POINTER(dbl), ctypes.POINTER(i64), ctypes.POINTER(i64), i32,
                                            i64, dbl]
             L.zo_scaler_update.restype = None
+            L.zo_sumsq_f32.argtypes = [P, i64]
+            L.zo_sumsq_f32.restype = dbl
+            L.zo_lamb.argtypes = [P, P, P, P, P, i64, P, i32, flt, ctypes.POINTER(Hyper), dbl, dbl, dbl, P]
+            L.zo_lamb.restype = ctypes.c_int
+            L.zo_lamb_step.argtypes = [P, P, P, P, P, i64, P, i32, dbl, dbl, dbl, dbl, dbl, i64, dbl, dbl, dbl,
+                                       dbl, ctypes.POINTER(Scalars), P]
+            L.zo_lamb_step.restype = ctypes.c_int
             _lib = L
     return _lib
 
@@ -177,6 +184,60 @@ def shard_step(g16, theta, m, v, p16, lr, beta1, beta2, eps, wd, t, loss_scale, 
                             _ptr(v, np.float32), _ptr(p16, np.uint16), n, lr, beta1, beta2, eps, wd, t,
                             loss_scale, clip, ctypes.byref(sc))
     return int(r), sc
+
+
+# --------------------------------------------------------------------------
+# LAMB (You et al.; listed by ZeRO's related work among the adaptive optimizers
+# whose memory ZeRO reduces)
+# --------------------------------------------------------------------------
+
+def sumsq_f32(x: np.ndarray) -> float:
+    """Exact sum of squares of a float32 array, rounded once to double."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return float(lib().zo_sumsq_f32(_ptr(x, np.float32), x.size))
+
+
+def _segments(seg_off, n):
+    off = np.ascontiguousarray(seg_off, dtype=np.int64)
+    if off.ndim != 1 or off.size < 1:
+        raise ValueError("seg_off must be a 1-D array of n_seg + 1 offsets")
+    return off, off.size - 1
+
+
+def lamb(g16, theta, m, v, p16, seg_off, mult: float, hp: Hyper, lr: float, phi_lo: float = 0.0,
+         phi_hi: float = float("inf")):
+    """In-place LAMB update on numpy arrays; returns an (n_seg, 3) array of
+    (sum theta^2, sum u^2, trust ratio) per layer."""
+    n = g16.size
+    for a in (theta, m, v, p16):
+        if a.size != n:
+            raise ValueError("shard arrays differ in length")
+    off, n_seg = _segments(seg_off, n)
+    out = np.empty((max(n_seg, 1), 3), np.float64)
+    r = lib().zo_lamb(_ptr(g16, np.uint16), _ptr(theta, np.float32), _ptr(m, np.float32), _ptr(v, np.float32),
+                      _ptr(p16, np.uint16), n, off.ctypes.data, n_seg, mult, ctypes.byref(hp), lr, phi_lo, phi_hi,
+                      out.ctypes.data)
+    if r != 0:
+        raise ValueError("malformed layer table")
+    return out[:n_seg]
+
+
+def lamb_step(g16, theta, m, v, p16, seg_off, lr, beta1, beta2, eps, wd, t, loss_scale, clip, phi_lo=0.0,
+              phi_hi=float("inf")):
+    """One whole LAMB step in place.  Returns (skipped, Scalars, per-layer array)."""
+    n = g16.size
+    for a in (theta, m, v, p16):
+        if a.size != n:
+            raise ValueError("shard arrays differ in length")
+    off, n_seg = _segments(seg_off, n)
+    out = np.zeros((max(n_seg, 1), 3), np.float64)
+    sc = Scalars()
+    r = lib().zo_lamb_step(_ptr(g16, np.uint16), _ptr(theta, np.float32), _ptr(m, np.float32), _ptr(v, np.float32),
+                           _ptr(p16, np.uint16), n, off.ctypes.data, n_seg, lr, beta1, beta2, eps, wd, t, loss_scale,
+                           clip, phi_lo, phi_hi, ctypes.byref(sc), out.ctypes.data)
+    if r < 0:
+        raise ValueError("malformed layer table")
+    return int(r), sc, out[:n_seg]
 
 
 # --------------------------------------------------------------------------

@@ -44,12 +44,21 @@
  *                     device for standard DP and the three ZeRO-DP stages.
  *   zo_scaler_update  Dynamic loss scaling (mixed-precision training): halve
  *                     on overflow, double after a window of good steps.
+ *   zo_sumsq_f32      The sum of squares of fp32 values taken EXACTLY in a
+ *                     640-bit fixed-point accumulator (every fp32 square is an
+ *                     integer multiple of 2^-298) and rounded once to double.
+ *   zo_lamb           LAMB (You et al.), a layer-wise adaptive optimizer that
+ *   zo_lamb_step      ZeRO's related work lists among the optimizers whose
+ *                     state partitioning makes affordable: Adam's moments,
+ *                     then each layer's update scaled by the trust ratio
+ *                     phi(||theta||)/||u|| with exact norms.
  *
  * Build: cc -std=gnu11 -O2 -ffp-contract=off -fno-fast-math -fPIC -shared
  * (x86-64: SSE arithmetic, so every float operation rounds once to fp32).
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 typedef unsigned __int128 zo_u128;
@@ -250,22 +259,30 @@ void zo_hyper(double lr, double beta1, double beta2, double eps, double wd, int6
  *   u     =  mhat / (sqrt(vhat) + eps)   [+ wd*theta, decoupled decay]
  *   theta <- theta - lr*u
  *   p16   =  binary16(theta) */
+/* The moments of one element and its update direction u (before any step
+ * size); shared by Adam and LAMB, which differ only in how u is scaled. */
+static float adam_direction(float g, float* m, float* v, float theta, const zo_hyper_t* h)
+{
+    float mi = h->b1 * *m + h->omb1 * g;
+    float vi = h->b2 * *v + h->omb2 * (g * g);
+    float mhat = mi / h->bc1;
+    float vhat = vi / h->bc2;
+    float denom = sqrtf(vhat) + h->eps;
+    float u = mhat / denom;
+    if (h->wd != 0.0f)
+        u = u + h->wd * theta;
+    *m = mi;
+    *v = vi;
+    return u;
+}
+
 void zo_adam(const uint16_t* g16, float* theta, float* m, float* v, uint16_t* p16, int64_t n,
              float mult, const zo_hyper_t* h)
 {
     for (int64_t i = 0; i < n; ++i) {
         float g = zo_f16_to_f32(g16[i]) * mult;
-        float mi = h->b1 * m[i] + h->omb1 * g;
-        float vi = h->b2 * v[i] + h->omb2 * (g * g);
-        float mhat = mi / h->bc1;
-        float vhat = vi / h->bc2;
-        float denom = sqrtf(vhat) + h->eps;
-        float u = mhat / denom;
-        if (h->wd != 0.0f)
-            u = u + h->wd * theta[i];
+        float u = adam_direction(g, &m[i], &v[i], theta[i], h);
         float th = theta[i] - h->lr * u;
-        m[i] = mi;
-        v[i] = vi;
         theta[i] = th;
         p16[i] = zo_f32_to_f16(th);
     }
@@ -339,4 +356,186 @@ void zo_scaler_update(double* scale, int64_t* applied, int64_t* good, int32_t sk
         *scale *= 2.0;
         *good = 0;
     }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Exact sum of squares of fp32 values                                       */
+/* ------------------------------------------------------------------------ */
+
+/* A finite binary32 x equals M * 2^E with integer 0 <= M < 2^24 and
+ * -149 <= E <= 104, so x^2 = M^2 * 2^(2E) is M^2 (below 2^48) shifted to bit
+ * 2E + 298 >= 0 of a fixed-point number whose unit is 2^-298.  The largest
+ * square reaches bit 554; 640 bits leave room for 2^85 terms.  Limbs are
+ * little-endian 64-bit words. */
+#define ZO_ACC_LIMBS 10
+
+typedef struct {
+    uint64_t limb[ZO_ACC_LIMBS];
+    int32_t has_inf, has_nan;
+} zo_acc_t;
+
+static void acc_add_at(zo_acc_t* a, uint64_t value, int bit)
+{
+    int q = bit / 64, r = bit % 64;
+    zo_u128 wide = (zo_u128)value << r;
+    uint64_t parts[2] = {(uint64_t)wide, (uint64_t)(wide >> 64)};
+    uint64_t carry = 0;
+    for (int i = q; i < ZO_ACC_LIMBS; ++i) {
+        zo_u128 s = (zo_u128)a->limb[i] + carry + (i - q < 2 ? parts[i - q] : 0);
+        a->limb[i] = (uint64_t)s;
+        carry = (uint64_t)(s >> 64);
+        if (i - q >= 1 && carry == 0)
+            break;
+    }
+}
+
+static void acc_add_square(zo_acc_t* a, float x)
+{
+    uint32_t b;
+    memcpy(&b, &x, 4);
+    uint32_t e = (b >> 23) & 255u, f = b & 0x7FFFFFu;
+    if (e == 255u) {
+        if (f)
+            a->has_nan = 1;
+        else
+            a->has_inf = 1;
+        return;
+    }
+    uint64_t M = e ? (f | 0x800000u) : f;
+    int E = e ? (int)e - 150 : -149;
+    if (M)
+        acc_add_at(a, M * M, 2 * E + 298);
+}
+
+/* The fixed-point value rounded once to the nearest double, ties to even. */
+static double acc_to_double(const zo_acc_t* a)
+{
+    if (a->has_nan)
+        return NAN;
+    if (a->has_inf)
+        return INFINITY;
+    int top = -1;
+    for (int i = ZO_ACC_LIMBS - 1; i >= 0 && top < 0; --i)
+        if (a->limb[i])
+            top = 64 * i + 63 - __builtin_clzll(a->limb[i]);
+    if (top < 0)
+        return 0.0;
+    if (top < 64)
+        return ldexp((double)a->limb[0], -298);  /* one 64-bit word: C rounds to nearest even */
+    /* the 64 bits [top-63, top] and whether anything below them is nonzero */
+    int lo = top - 63, q = lo / 64, r = lo % 64;
+    uint64_t head = a->limb[q] >> r;
+    if (r)
+        head |= a->limb[q + 1] << (64 - r);
+    int sticky = r ? (a->limb[q] & ((1ull << r) - 1)) != 0 : 0;
+    for (int i = 0; i < q && !sticky; ++i)
+        sticky = a->limb[i] != 0;
+    uint64_t mant = head >> 11, rem = head & 0x7FFu;
+    if (rem > 0x400u || (rem == 0x400u && (sticky || (mant & 1u))))
+        mant += 1;  /* may reach 2^53, still exact as a double */
+    return ldexp((double)mant, lo + 11 - 298);
+}
+
+/* sum of x[i]^2 over i < n, exact, then rounded once to double; +inf if an
+ * element is infinite, NaN if one is NaN. */
+double zo_sumsq_f32(const float* x, int64_t n)
+{
+    zo_acc_t a;
+    memset(&a, 0, sizeof a);
+    for (int64_t i = 0; i < n; ++i)
+        acc_add_square(&a, x[i]);
+    return acc_to_double(&a);
+}
+
+/* ------------------------------------------------------------------------ */
+/* LAMB: Adam's moments with a per-layer trust ratio                         */
+/* ------------------------------------------------------------------------ */
+
+/* Layer-wise adaptive large-batch optimization (You et al., LAMB, one of the
+ * adaptive optimizers ZeRO's related-work section lists as made affordable by
+ * partitioning the optimizer state).  The flat vector is cut into layers
+ * [seg_off[s], seg_off[s+1]).  Per element, in fp32, exactly as zo_adam up to
+ * the update direction:
+ *   m <- b1*m + (1-b1)*g;  v <- b2*v + (1-b2)*g^2
+ *   u  = (m/(1-b1^t)) / (sqrt(v/(1-b2^t)) + eps)   [+ wd*theta]
+ * then per layer, with the norms of the layer's old theta and of u taken
+ * exactly and rounded once to double:
+ *   trust = phi(||theta||) / ||u||   (1 when either norm is zero),
+ *   phi(z) = min(max(z, phi_lo), phi_hi),
+ *   step   = (float)(lr * trust)      (computed in double, rounded once)
+ *   theta <- theta - step*u;  p16 = binary16(theta).
+ * seg_out (3 doubles per layer, may be NULL) receives sum theta^2, sum u^2
+ * and the trust ratio.  Returns 0, or -1 on a malformed layer table
+ * (seg_off must rise strictly from 0 to n) or an allocation failure. */
+int zo_lamb(const uint16_t* g16, float* theta, float* m, float* v, uint16_t* p16, int64_t n,
+            const int64_t* seg_off, int32_t n_seg, float mult, const zo_hyper_t* h, double lr,
+            double phi_lo, double phi_hi, double* seg_out)
+{
+    if (n_seg < 0 || (n_seg == 0 && n != 0) || (n_seg > 0 && (seg_off[0] != 0 || seg_off[n_seg] != n)))
+        return -1;
+    int64_t longest = 0;
+    for (int32_t s = 0; s < n_seg; ++s) {
+        if (seg_off[s + 1] <= seg_off[s])
+            return -1;
+        if (seg_off[s + 1] - seg_off[s] > longest)
+            longest = seg_off[s + 1] - seg_off[s];
+    }
+    float* u = (float*)malloc((size_t)(longest ? longest : 1) * sizeof(float));
+    if (!u)
+        return -1;
+    for (int32_t s = 0; s < n_seg; ++s) {
+        const int64_t a = seg_off[s], len = seg_off[s + 1] - a;
+        for (int64_t j = 0; j < len; ++j) {
+            const int64_t i = a + j;
+            float g = zo_f16_to_f32(g16[i]) * mult;
+            u[j] = adam_direction(g, &m[i], &v[i], theta[i], h);
+        }
+        const double st = zo_sumsq_f32(theta + a, len);
+        const double su = zo_sumsq_f32(u, len);
+        double trust = 1.0;
+        if (st > 0.0 && su > 0.0) {
+            double wn = sqrt(st);
+            if (wn < phi_lo)
+                wn = phi_lo;
+            if (wn > phi_hi)
+                wn = phi_hi;
+            trust = wn / sqrt(su);
+        }
+        const float step = (float)(lr * trust);
+        for (int64_t j = 0; j < len; ++j) {
+            const int64_t i = a + j;
+            float th = theta[i] - step * u[j];
+            theta[i] = th;
+            p16[i] = zo_f32_to_f16(th);
+        }
+        if (seg_out) {
+            seg_out[3 * s] = st;
+            seg_out[3 * s + 1] = su;
+            seg_out[3 * s + 2] = trust;
+        }
+    }
+    free(u);
+    return 0;
+}
+
+/* The whole LAMB step: gradient statistics and scalars as for Adam, then
+ * skip (returns 1, nothing written) or the update (returns 0); -1 on a
+ * malformed layer table. */
+int zo_lamb_step(const uint16_t* g16, float* theta, float* m, float* v, uint16_t* p16, int64_t n,
+                 const int64_t* seg_off, int32_t n_seg, double lr, double beta1, double beta2, double eps,
+                 double wd, int64_t t, double loss_scale, double clip, double phi_lo, double phi_hi,
+                 zo_scalars_t* out, double* seg_out)
+{
+    uint64_t s[2];
+    int32_t ovf;
+    zo_scalars_t sc;
+    zo_local_stats(g16, n, s, &ovf);
+    zo_scalars(s, ovf, loss_scale, clip, &sc);
+    if (out)
+        *out = sc;
+    if (sc.skip != 0)
+        return 1;
+    zo_hyper_t h;
+    zo_hyper(lr, beta1, beta2, eps, wd, t, &h);
+    return zo_lamb(g16, theta, m, v, p16, n, seg_off, n_seg, sc.mult, &h, lr, phi_lo, phi_hi, seg_out);
 }

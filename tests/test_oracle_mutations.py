@@ -18,18 +18,19 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "zero_oracle.c")
 PIN_TESTS = ["tests/test_oracle_accounting.py", "tests/test_oracle_layout.py", "tests/test_oracle_binary16.py",
-             "tests/test_oracle_stats.py", "tests/test_oracle_adam.py", "tests/test_oracle_invariants.py"]
+             "tests/test_oracle_stats.py", "tests/test_oracle_adam.py", "tests/test_oracle_invariants.py",
+             "tests/test_oracle_lamb.py"]
 
 MUTANTS = {
     "update_sign": ("float th = theta[i] - h->lr * u;", "float th = theta[i] + h->lr * u;"),
     "bias_correction_swapped": ("float mhat = mi / h->bc1;", "float mhat = mi / h->bc2;"),
     "eps_inside_sqrt": ("float denom = sqrtf(vhat) + h->eps;", "float denom = sqrtf(vhat + h->eps);"),
     "variance_not_squared": ("h->omb2 * (g * g);", "h->omb2 * g;"),
-    "variance_decay_beta1": ("float vi = h->b2 * v[i]", "float vi = h->b1 * v[i]"),
+    "variance_decay_beta1": ("float vi = h->b2 * *v", "float vi = h->b1 * *v"),
     "bias_t_off_by_one": ("h->bc1 = (float)(1.0 - pow(beta1, (double)t));",
                           "h->bc1 = (float)(1.0 - pow(beta1, (double)(t + 1)));"),
     "no_bias_correction_v": ("h->bc2 = (float)(1.0 - pow(beta2, (double)t));", "h->bc2 = 1.0f;"),
-    "decay_sign": ("u = u + h->wd * theta[i];", "u = u - h->wd * theta[i];"),
+    "decay_sign": ("u = u + h->wd * theta;", "u = u - h->wd * theta;"),
     "clip_inverted": ("clip / out->norm : 1.0;", "out->norm / clip : 1.0;"),
     "unscale_multiplies": ("out->mult = (float)(out->coef / loss_scale);",
                            "out->mult = (float)(out->coef * loss_scale);"),
@@ -46,6 +47,27 @@ MUTANTS = {
     "writes_on_skip": ("    if (sc.skip)\n        return 1;\n", ""),
     "scaler_no_halving": ("double s = *scale / 2.0;", "double s = *scale;"),
     "t_counts_skips": ("        *good = 0;\n        return;\n", "        *good = 0;\n        *applied += 1;\n        return;\n"),
+    # exact fp32 sum of squares
+    "acc_drops_carry": ("        if (i - q >= 1 && carry == 0)\n", "        if (i - q >= 1)\n"),
+    "acc_carry_not_added": ("zo_u128 s = (zo_u128)a->limb[i] + carry + (i - q < 2 ? parts[i - q] : 0);",
+                            "zo_u128 s = (zo_u128)a->limb[i] + (i - q < 2 ? parts[i - q] : 0);"),
+    "acc_ignores_sticky": ("(rem == 0x400u && (sticky || (mant & 1u)))", "(rem == 0x400u && (mant & 1u))"),
+    "acc_ties_away": ("(rem == 0x400u && (sticky || (mant & 1u)))", "(rem == 0x400u)"),
+    "acc_subnormal_exponent": ("int E = e ? (int)e - 150 : -149;", "int E = e ? (int)e - 150 : -150;"),
+    "acc_implicit_bit": ("uint64_t M = e ? (f | 0x800000u) : f;", "uint64_t M = f;"),
+    # LAMB
+    "lamb_trust_inverted": ("trust = wn / sqrt(su);", "trust = sqrt(su) / wn;"),
+    "lamb_weight_norm_squared": ("double wn = sqrt(st);", "double wn = st;"),
+    "lamb_zero_norm_freezes": ("        double trust = 1.0;\n", "        double trust = 0.0;\n"),
+    "lamb_phi_upper_uses_lower": ("            if (wn > phi_hi)\n                wn = phi_hi;\n",
+                                  "            if (wn > phi_hi)\n                wn = phi_lo;\n"),
+    "lamb_phi_lower_ignored": ("            if (wn < phi_lo)\n                wn = phi_lo;\n", ""),
+    "lamb_layer_tail_skipped": ("        for (int64_t j = 0; j < len; ++j) {\n            const int64_t i = a + j;\n            float g",
+                                "        for (int64_t j = 0; j < len - 1; ++j) {\n            const int64_t i = a + j;\n            float g"),
+    "lamb_writes_on_skip": ("    if (sc.skip != 0)\n        return 1;\n", ""),
+    "lamb_applies_adam_step": ("float th = theta[i] - step * u[j];", "float th = theta[i] - h->lr * u[j];"),
+    "lamb_norm_over_whole_vector": ("const double st = zo_sumsq_f32(theta + a, len);",
+                                    "const double st = zo_sumsq_f32(theta, n);"),
 }
 
 
