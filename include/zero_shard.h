@@ -206,6 +206,86 @@ int zero_scaler_update(zero_scaler_t* s, int32_t skipped);
 int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, double* out);
 
 /* ------------------------------------------------------------------------ */
+/* LAMB: the same mixed-precision shard step with a per-layer trust ratio    */
+/* ------------------------------------------------------------------------ */
+
+/* LAMB (You et al., layer-wise adaptive moments for large batches) is among
+ * the adaptive optimizers that ZeRO's related work (Sec. 2.3) says its
+ * partitioning of optimizer state makes affordable.  Its fp32 state is Adam's
+ * (K = 12, Sec. 3.1); only the update differs.  With the moments and the
+ * direction u of zero_shard_step (unscale + clip, bias correction, eps outside
+ * the square root, decoupled weight decay), each layer L of the shard moves by
+ *     theta_L <- theta_L - step_L * u_L,
+ *     step_L   = (float)(lr * trust_L)   (computed in double, rounded once),
+ *     trust_L  = phi(||theta_L||) / ||u_L||, or 1 if either norm is zero,
+ *     phi(z)   = min(max(z, phi_lo), phi_hi)   (phi_lo = 0, phi_hi = +inf:
+ *                identity),
+ * where the norms are over the layer's old parameters and its whole u.
+ *
+ * A plan holds the shard's layer table and the work decomposition built from
+ * it.  seg_off (HOST memory, n_seg + 1 int64 offsets, copied) must rise
+ * strictly from seg_off[0] = 0 to seg_off[n_seg] = n: layer s is elements
+ * [seg_off[s], seg_off[s+1]) of the shard.  n = 0 requires n_seg = 0.  A
+ * layer that continues on a neighbouring rank's shard appears clipped to this
+ * shard; its norms then need the split-phase calls below.  The plan is tied to
+ * the device current at creation and owns device memory (about 16 bytes per
+ * 256 elements plus 32 bytes per layer, and the work lists, built per array
+ * alignment on first use); zero_lamb_plan_destroy waits for the device and
+ * frees it.  Calls on one plan are serialised by the library; a call on a
+ * different stream from the plan's previous call first waits for that stream.
+ * Returns ZERO_OK, ZERO_EINVAL (bad table, n outside [0, 2^40], NULL out) or
+ * ZERO_ENOMEM / ZERO_EHIP. */
+typedef struct zero_lamb_plan zero_lamb_plan_t;
+
+int zero_lamb_plan_create(const int64_t* seg_off, int32_t n_seg, int64_t n, zero_lamb_plan_t** out);
+int zero_lamb_plan_destroy(zero_lamb_plan_t* plan);
+
+/* One LAMB step on a shard whose layers all lie in it (N_d = 1, or a caller
+ * that cuts its flat buffer at layer boundaries).  Arrays, checks, skip
+ * semantics, return values and zero_shard_last_stats as for zero_shard_step,
+ * with n taken from the plan; phi_lo >= 0, phi_hi >= phi_lo (may be +inf),
+ * neither NaN.  The library's per-layer sums live in the plan. */
+int zero_lamb_step(const zero_lamb_plan_t* plan, const uint16_t* grad16, float* master32, float* m32, float* v32,
+                   uint16_t* param16_out, double lr, double beta1, double beta2, double eps, double weight_decay,
+                   int64_t step, double loss_scale, double clip, double phi_lo, double phi_hi, void* stream);
+
+/* Split phase for layers that straddle shards (Sec. 5.1 cuts the flat buffer
+ * without regard to layers):
+ *   1. zero_shard_stats -> the ranks combine the gradient sums (global_sumsq);
+ *   2. zero_lamb_moments writes m and v and, into layer_sumsq (DEVICE, 2*n_seg
+ *      doubles, 16-byte aligned, caller-owned), this shard's sum theta^2 and
+ *      sum u^2 of each local layer;
+ *   3. the caller adds, for every layer shared with a neighbouring rank, the
+ *      neighbours' entries of that layer (rank order), in place;
+ *   4. zero_lamb_apply updates theta and the fp16 copy from the moments
+ *      stored in step 2 and the completed layer sums.
+ * Both calls take the same hyperparameters and global_sumsq; a non-finite
+ * global_sumsq (gradient overflow on some rank) returns ZERO_SKIPPED from both
+ * without launching anything. */
+int zero_lamb_moments(const zero_lamb_plan_t* plan, const uint16_t* grad16, const float* master32, float* m32,
+                      float* v32, double global_sumsq, double beta1, double beta2, double eps, double weight_decay,
+                      int64_t step, double loss_scale, double clip, double* layer_sumsq, void* stream);
+int zero_lamb_apply(const zero_lamb_plan_t* plan, float* master32, const float* m32, const float* v32,
+                    uint16_t* param16_out, double global_sumsq, const double* layer_sumsq, double lr, double beta1,
+                    double beta2, double eps, double weight_decay, int64_t step, double phi_lo, double phi_hi,
+                    void* stream);
+
+/* Kernel timing of sampled zero_lamb_step calls (the sampling period is the
+ * one zero_profile_enable sets): events before the statistics, moments,
+ * layer-sum and apply kernels and after the last.  zero_lamb_profile_read
+ * waits for the recorded work, returns the sums since the last read and resets
+ * them. */
+typedef struct {
+    int64_t steps;      /* steps timed                                  */
+    double stats_ms;    /* statistics + finalize kernels                */
+    double moments_ms;  /* k_lamb_moments                               */
+    double layer_ms;    /* k_lamb_layer                                 */
+    double apply_ms;    /* k_lamb_apply                                 */
+} zero_lamb_profile_t;
+
+int zero_lamb_profile_read(zero_lamb_profile_t* out);
+
+/* ------------------------------------------------------------------------ */
 /* Diagnostics                                                              */
 /* ------------------------------------------------------------------------ */
 

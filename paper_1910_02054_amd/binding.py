@@ -45,6 +45,11 @@ class Profile(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("update_ms", ctypes.c_double)]
 
 
+class LambProfile(ctypes.Structure):
+    _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("moments_ms", ctypes.c_double),
+                ("layer_ms", ctypes.c_double), ("apply_ms", ctypes.c_double)]
+
+
 _P, _i64, _i32, _dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
 _lib.zero_partition_layout.argtypes = [_i64, _i32, _i32, ctypes.POINTER(Layout)]
 _lib.zero_shard_step.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
@@ -60,16 +65,24 @@ _lib.zero_last_error.restype = ctypes.c_char_p
 _lib.zero_profile_enable.argtypes = [_i32]
 _lib.zero_profile_read.argtypes = [ctypes.POINTER(Profile)]
 _lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
+_lib.zero_lamb_plan_create.argtypes = [_P, _i32, _i64, ctypes.POINTER(_P)]
+_lib.zero_lamb_plan_destroy.argtypes = [_P]
+_lib.zero_lamb_step.argtypes = [_P, _P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _dbl, _dbl, _P]
+_lib.zero_lamb_moments.argtypes = [_P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P, _P]
+_lib.zero_lamb_apply.argtypes = [_P, _P, _P, _P, _P, _dbl, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
+_lib.zero_lamb_profile_read.argtypes = [ctypes.POINTER(LambProfile)]
 for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
            "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
-           "zero_probe_copy"):
+           "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step",
+           "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
            "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
-           "zero_profile_read", "zero_probe_copy")
+           "zero_profile_read", "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy",
+           "zero_lamb_step", "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read")
 
 
 def _check(rc):
@@ -214,6 +227,102 @@ def zero_probe_copy(src, dst, nbytes=None, stream=None):
     if nbytes is None:
         nbytes = src.numel() * src.element_size()
     _check(_lib.zero_probe_copy(_addr(src), _addr(dst), int(nbytes), _stream(stream)))
+
+
+class LambPlan:
+    """A LAMB layer-table plan (zero_lamb_plan_t) on the current device.
+
+    seg_off: the n_seg + 1 layer offsets of the shard (any int sequence or
+    int64 array, copied by the library); n = seg_off[-1]."""
+
+    def __init__(self, seg_off):
+        import numpy as np
+        off = np.ascontiguousarray(np.asarray(seg_off, dtype=np.int64))
+        if off.ndim != 1 or off.size < 1:
+            raise ValueError("seg_off must be a 1-D sequence of n_seg + 1 offsets")
+        self.n = int(off[-1])
+        self.n_seg = off.size - 1
+        h = _P()
+        _check(_lib.zero_lamb_plan_create(off.ctypes.data, self.n_seg, self.n, ctypes.byref(h)))
+        self._h = h
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            h, self._h = self._h, None
+            _check(_lib.zero_lamb_plan_destroy(h))
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _lamb_check_len(plan, *tensors):
+    for t in tensors:
+        if t is not None and not isinstance(t, int) and t.numel() != plan.n:
+            raise ValueError("shard tensors must have the plan's n = %d elements" % plan.n)
+
+
+def zero_lamb_step(plan, grad16, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, step,
+                   loss_scale, clip, phi_lo=0.0, phi_hi=float("inf"), stream=None) -> int:
+    """One LAMB step over the plan's layers; 0 applied, 1 skipped (overflow)."""
+    import torch
+    h16, f32 = (torch.float16, torch.int16), (torch.float32,)
+    _lamb_check_len(plan, grad16, master32, m32, v32, param16_out)
+    return _check(_lib.zero_lamb_step(
+        plan.handle, _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), float(lr), float(beta1), float(beta2),
+        float(eps), float(weight_decay), int(step), float(loss_scale), float(clip), float(phi_lo), float(phi_hi),
+        _stream(stream)))
+
+
+def zero_lamb_moments(plan, grad16, master32, m32, v32, global_sumsq, beta1, beta2, eps, weight_decay, step,
+                      loss_scale, clip, layer_sumsq, stream=None) -> int:
+    """Split phase, part 1: moments and this shard's per-layer sums into
+    layer_sumsq (a float64 device tensor of 2*n_seg elements)."""
+    import torch
+    h16, f32 = (torch.float16, torch.int16), (torch.float32,)
+    _lamb_check_len(plan, grad16, master32, m32, v32)
+    if not isinstance(layer_sumsq, int) and layer_sumsq.numel() != 2 * plan.n_seg:
+        raise ValueError("layer_sumsq must hold 2 * n_seg = %d doubles" % (2 * plan.n_seg))
+    return _check(_lib.zero_lamb_moments(
+        plan.handle, _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), float(global_sumsq), float(beta1), float(beta2), float(eps), float(weight_decay),
+        int(step), float(loss_scale), float(clip), _addr(layer_sumsq, (torch.float64,), "layer_sumsq"),
+        _stream(stream)))
+
+
+def zero_lamb_apply(plan, master32, m32, v32, param16_out, global_sumsq, layer_sumsq, lr, beta1, beta2, eps,
+                    weight_decay, step, phi_lo=0.0, phi_hi=float("inf"), stream=None) -> int:
+    """Split phase, part 2: the update from the stored moments and the completed layer sums."""
+    import torch
+    h16, f32 = (torch.float16, torch.int16), (torch.float32,)
+    _lamb_check_len(plan, master32, m32, v32, param16_out)
+    if not isinstance(layer_sumsq, int) and layer_sumsq.numel() != 2 * plan.n_seg:
+        raise ValueError("layer_sumsq must hold 2 * n_seg = %d doubles" % (2 * plan.n_seg))
+    return _check(_lib.zero_lamb_apply(
+        plan.handle, _addr(master32, f32, "master32"), _addr(m32, f32, "m32"), _addr(v32, f32, "v32"),
+        _addr(param16_out, h16, "param16_out"), float(global_sumsq), _addr(layer_sumsq, (torch.float64,),
+                                                                           "layer_sumsq"),
+        float(lr), float(beta1), float(beta2), float(eps), float(weight_decay), int(step), float(phi_lo),
+        float(phi_hi), _stream(stream)))
+
+
+def zero_lamb_profile_read() -> LambProfile:
+    out = LambProfile()
+    _check(_lib.zero_lamb_profile_read(ctypes.byref(out)))
+    return out
 
 
 def raw_library():

@@ -218,9 +218,9 @@ __global__ __launch_bounds__(BLOCK) void k_stats(const uint16_t* __restrict__ g,
 // ---------------------------------------------------------------------------
 constexpr int kFinalBlock = 256;
 
-__global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restrict__ part, int nparts,
-                                                          Result* __restrict__ res, Result* __restrict__ res_host,
-                                                          double loss_scale, double clip, uint32_t seq) {
+[[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize(
+    const Partial* __restrict__ part, int nparts, Result* __restrict__ res, Result* __restrict__ res_host,
+    double loss_scale, double clip, uint32_t seq) {
     double s0 = 0.0, s1 = 0.0;
     int i = threadIdx.x;
     for (; i + kFinalBlock < nparts; i += 2 * kFinalBlock) {
@@ -244,8 +244,9 @@ __global__ __launch_bounds__(kFinalBlock) void k_finalize(const Partial* __restr
 
 // Result record from a global sum of squares supplied by the caller (the
 // split-phase step: each rank's local sums combined outside the library).
-__global__ __launch_bounds__(64) void k_set_result(Result* __restrict__ res, double global_sumsq, double loss_scale,
-                                                   double clip, uint32_t seq) {
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_result(Result* __restrict__ res,
+                                                                            double global_sumsq, double loss_scale,
+                                                                            double clip, uint32_t seq) {
     if (threadIdx.x == 0)
         *res = make_result(global_sumsq, loss_scale, clip, seq);
 }
@@ -349,11 +350,9 @@ __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__
 }
 
 // K2 (scalar path) for arrays whose element misalignments differ.
-__global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(const uint16_t* __restrict__ g,
-                                                              float* __restrict__ th, float* __restrict__ m,
-                                                              float* __restrict__ v, uint16_t* __restrict__ p,
-                                                              int64_t n, const Result* __restrict__ res,
-                                                              AdamConst c) {
+[[maybe_unused]] static __global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
+    const uint16_t* __restrict__ g, float* __restrict__ th, float* __restrict__ m, float* __restrict__ v,
+    uint16_t* __restrict__ p, int64_t n, const Result* __restrict__ res, AdamConst c) {
     if (res->skip)
         return;
     const float mult = res->mult;

@@ -1,0 +1,560 @@
+// zero_lamb.hip -- host side of the LAMB shard step (declared in
+// include/zero_shard.h): the layer-table plan and its work lists, argument
+// checks, launches, split-phase entry points and sampled kernel timing.
+//
+// LAMB (You et al.) is listed in ZeRO's related work (Sec. 2.3) among the
+// adaptive optimizers whose state ZeRO's partitioning (Sec. 5.1-5.2) makes
+// affordable; the fp32 state per parameter is Adam's (Sec. 3.1, K = 12).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <mutex>
+#include <vector>
+
+#include "zero_shard.h"
+#include "shard_kernels.hpp"
+#include "lamb_kernels.hpp"
+#include "host_common.hpp"
+
+// ---------------------------------------------------------------------------
+// Launch policy of the two LAMB streaming passes (template knobs in
+// lamb_kernels.hpp): one tile of BLOCK*U 4-element vectors per work item, at
+// most kLambPerCU resident workgroups per CU (an LDS reservation).
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kLambBlock = 64, kLambUnroll = 1, kLambPerCU = 12;
+constexpr bool kLambNTL = true, kLambNTS = true;
+constexpr int64_t kLambTile = 4 * (int64_t)kLambBlock * kLambUnroll;  // elements per tile
+constexpr int64_t kLambMaxBlocks = 1 << 26;
+constexpr int kPhases = 5;  // vector paths for element misalignment 0..3, then the scalar path
+}  // namespace
+
+using namespace zsh;
+
+// The work list of one array alignment: items (with the end sentinel) and the
+// first item of every layer (with the end sentinel), on the device.
+struct LambWork {
+    zs::LambItem* items = nullptr;
+    int64_t* first = nullptr;
+    int64_t n_items = 0;
+    bool built = false;
+};
+
+struct LambProfRec {
+    hipEvent_t e[5];
+};
+
+struct zero_lamb_plan {
+    std::mutex mu;
+    int dev = 0;
+    int64_t n = 0;
+    int32_t n_seg = 0;
+    std::vector<int64_t> seg_off;
+    LambWork work[kPhases];
+    zs::LayerSums* part = nullptr;  // one partial per item (sized for the longest list)
+    zs::LayerSums* sums = nullptr;  // per-layer sums of zero_lamb_step
+    int64_t max_items = 0;
+    hipStream_t last_stream = nullptr;
+    bool used = false;
+    uint64_t prof_tick = 0;
+    size_t lds[2] = {0, 0};  // occupancy reservations of the moments and apply kernels (per phase kind)
+    size_t lds_scalar[2] = {0, 0};
+};
+
+namespace {
+
+std::mutex g_lprof_mu;
+std::vector<LambProfRec> g_lprof_pending;
+std::vector<hipEvent_t> g_lprof_pool;
+zero_lamb_profile_t g_lprof_acc = {0, 0.0, 0.0, 0.0, 0.0};
+
+template <bool VEC>
+const void* moments_kernel() {
+    return reinterpret_cast<const void*>(zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC>);
+}
+template <bool VEC>
+const void* apply_kernel() {
+    return reinterpret_cast<const void*>(zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC>);
+}
+
+// Upper bound on the items of any alignment: one per tile the shard touches
+// (at most n/T + 2, counting the partial tile below the first aligned vector)
+// plus one per interior layer boundary.
+int64_t max_items_for(int64_t n, int32_t n_seg) { return n / kLambTile + 2 + (int64_t)n_seg; }
+
+// Cut [0, n) at tile boundaries (head + k*T, plus 0) and at layer boundaries.
+void build_items(const std::vector<int64_t>& off, int32_t n_seg, int64_t head, std::vector<zs::LambItem>* items,
+                 std::vector<int64_t>* first) {
+    items->clear();
+    first->assign((size_t)n_seg + 1, 0);
+    for (int32_t s = 0; s < n_seg; ++s) {
+        (*first)[s] = (int64_t)items->size();
+        int64_t pos = off[s];
+        const int64_t end = off[s + 1];
+        while (pos < end) {
+            int64_t tile_end;
+            if (pos < head)
+                tile_end = head;
+            else
+                tile_end = head + ((pos - head) / kLambTile + 1) * kLambTile;
+            items->push_back(zs::LambItem{pos, s, 0});
+            pos = tile_end < end ? tile_end : end;
+        }
+    }
+    (*first)[n_seg] = (int64_t)items->size();
+    const int64_t n = n_seg ? off[n_seg] : 0;
+    items->push_back(zs::LambItem{n, -1, 0});
+}
+
+// The work list of `phase` (0..3: vector path with that head; 4: scalar path),
+// built and uploaded on first use.  Caller holds plan->mu.
+int get_work(zero_lamb_plan* plan, int phase, LambWork** out) {
+    LambWork& w = plan->work[phase];
+    if (!w.built) {
+        std::vector<zs::LambItem> items;
+        std::vector<int64_t> first;
+        const int64_t head = phase < 4 ? phase : 0;  // the kernels take the same head
+        build_items(plan->seg_off, plan->n_seg, head, &items, &first);
+        const int64_t n_items = (int64_t)items.size() - 1;
+        if (n_items > plan->max_items)
+            return fail(ZERO_EHIP, "zero_lamb: work list of %lld items exceeds the bound %lld", (long long)n_items,
+                        (long long)plan->max_items);
+        if (hipMalloc(reinterpret_cast<void**>(&w.items), items.size() * sizeof(zs::LambItem)) != hipSuccess ||
+            hipMalloc(reinterpret_cast<void**>(&w.first), first.size() * sizeof(int64_t)) != hipSuccess) {
+            if (w.items) (void)hipFree(w.items);
+            w.items = nullptr;
+            (void)hipGetLastError();
+            return fail(ZERO_ENOMEM, "zero_lamb: could not allocate a work list of %lld items", (long long)n_items);
+        }
+        HIP_TRY(hipMemcpy(w.items, items.data(), items.size() * sizeof(zs::LambItem), hipMemcpyHostToDevice));
+        HIP_TRY(hipMemcpy(w.first, first.data(), first.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+        w.n_items = n_items;
+        w.built = true;
+    }
+    *out = &w;
+    return ZERO_OK;
+}
+
+// Element misalignment shared by all arrays (0..3), or 4 when they differ (or
+// when an fp16 array is only 2-byte aligned relative to its fp32 partners).
+int phase_of(const uint16_t* g, const float* th, const float* m, const float* v, const uint16_t* p) {
+    const uintptr_t ef[3] = {(reinterpret_cast<uintptr_t>(th) & 15) / 4, (reinterpret_cast<uintptr_t>(m) & 15) / 4,
+                             (reinterpret_cast<uintptr_t>(v) & 15) / 4};
+    bool same = ef[0] == ef[1] && ef[0] == ef[2];
+    if (g)
+        same = same && (reinterpret_cast<uintptr_t>(g) & 7) / 2 == ef[0];
+    if (p)
+        same = same && (reinterpret_cast<uintptr_t>(p) & 7) / 2 == ef[0];
+    return same ? (int)((4 - ef[0]) & 3) : 4;
+}
+
+int check_plan(const char* fn, const zero_lamb_plan_t* plan) {
+    if (!plan)
+        return fail(ZERO_EINVAL, "%s: NULL plan", fn);
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev != plan->dev)
+        return fail(ZERO_EINVAL, "%s: plan was created on device %d, current device is %d", fn, plan->dev, dev);
+    return ZERO_OK;
+}
+
+int check_phi(const char* fn, double phi_lo, double phi_hi) {
+    if (std::isnan(phi_lo) || std::isnan(phi_hi) || !(phi_lo >= 0.0) || !(phi_hi >= phi_lo) || std::isinf(phi_lo))
+        return fail(ZERO_EINVAL, "%s: need 0 <= phi_lo <= phi_hi (phi_hi may be +inf)", fn);
+    return ZERO_OK;
+}
+
+// Alignment, NULL, overlap and allocation checks of the arrays a call touches
+// (NULL entries of ptrs are arrays the call does not take).
+int check_lamb_arrays(const char* fn, const void* const ptrs[5], int64_t n) {
+    static const size_t esz[5] = {2, 4, 4, 4, 2};
+    size_t bytes[5];
+    const void* live[5];
+    size_t live_bytes[5];
+    int k = 0;
+    for (int i = 0; i < 5; ++i) {
+        bytes[i] = esz[i] * (size_t)n;
+        if (!ptrs[i])
+            continue;
+        if (reinterpret_cast<uintptr_t>(ptrs[i]) % esz[i])
+            return fail(ZERO_EINVAL, "%s: array %d is not %zu-byte aligned", fn, i, esz[i]);
+        live[k] = ptrs[i];
+        live_bytes[k] = bytes[i];
+        ++k;
+    }
+    if (n == 0)
+        return ZERO_OK;
+    for (int i = 0; i < 5; ++i)
+        for (int j = i + 1; j < 5; ++j)
+            if (ptrs[i] && ptrs[j] &&
+                overlaps(reinterpret_cast<uintptr_t>(ptrs[i]), bytes[i], reinterpret_cast<uintptr_t>(ptrs[j]),
+                         bytes[j]))
+                return fail(ZERO_EINVAL, "%s: arrays %d and %d overlap", fn, i, j);
+    return check_ranges(fn, live, live_bytes, k);
+}
+
+int check_layer_sums(const char* fn, const zero_lamb_plan_t* plan, const void* layer_sumsq,
+                     const void* const arrays[5]) {
+    if (!layer_sumsq || reinterpret_cast<uintptr_t>(layer_sumsq) % 16)
+        return fail(ZERO_EINVAL, "%s: layer_sumsq must be a 16-byte aligned device array", fn);
+    const size_t bytes = 16 * (size_t)plan->n_seg;
+    for (int i = 0; i < 5; ++i)
+        if (arrays[i] && overlaps(reinterpret_cast<uintptr_t>(arrays[i]), (i == 0 || i == 4 ? 2 : 4) * (size_t)plan->n,
+                                  reinterpret_cast<uintptr_t>(layer_sumsq), bytes))
+            return fail(ZERO_EINVAL, "%s: layer_sumsq overlaps array %d", fn, i);
+    return check_ranges(fn, &layer_sumsq, &bytes, 1);
+}
+
+// Work queued on the plan's previous stream must finish before another
+// stream reuses the plan's partials and sums.
+int switch_stream(zero_lamb_plan* plan, hipStream_t stream) {
+    if (plan->used && plan->last_stream != stream)
+        HIP_TRY(hipStreamSynchronize(plan->last_stream));
+    plan->used = true;
+    plan->last_stream = stream;
+    return ZERO_OK;
+}
+
+unsigned grid_for(int64_t n_items) {
+    int64_t b = n_items < 1 ? 1 : n_items;
+    return (unsigned)(b > kLambMaxBlocks ? kLambMaxBlocks : b);
+}
+
+int launch_moments(zero_lamb_plan* plan, const LambWork& w, int phase, const uint16_t* g, const float* th, float* m,
+                   float* v, const zs::Result* res, const zs::AdamConst& c, hipStream_t stream) {
+    const unsigned grid = grid_for(w.n_items);
+    if (phase < 4)
+        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
+            <<<grid, kLambBlock, plan->lds[0], stream>>>(g, th, m, v, w.items, w.n_items, phase, res, c, plan->part);
+    else
+        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
+            <<<grid, kLambBlock, plan->lds_scalar[0], stream>>>(g, th, m, v, w.items, w.n_items, 0, res, c,
+                                                                 plan->part);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+int launch_layer(zero_lamb_plan* plan, const LambWork& w, zs::LayerSums* sums, const zs::Result* res,
+                 hipStream_t stream) {
+    const int64_t g = plan->n_seg < 1 ? 1 : (plan->n_seg > kLambMaxBlocks ? kLambMaxBlocks : plan->n_seg);
+    zs::k_lamb_layer<<<(unsigned)g, zs::kLayerBlock, 0, stream>>>(plan->part, w.first, plan->n_seg, sums, res);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+int launch_apply(zero_lamb_plan* plan, const LambWork& w, int phase, float* th, const float* m, const float* v,
+                 uint16_t* p, const zs::LayerSums* sums, const zs::Result* res, const zs::AdamConst& c, double lr,
+                 double phi_lo, double phi_hi, hipStream_t stream) {
+    const unsigned grid = grid_for(w.n_items);
+    if (phase < 4)
+        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
+            <<<grid, kLambBlock, plan->lds[1], stream>>>(th, m, v, p, w.items, w.n_items, phase, sums, res, c, lr,
+                                                         phi_lo, phi_hi);
+    else
+        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
+            <<<grid, kLambBlock, plan->lds_scalar[1], stream>>>(th, m, v, p, w.items, w.n_items, 0, sums, res, c, lr,
+                                                                 phi_lo, phi_hi);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+hipEvent_t lprof_event() {
+    if (!g_lprof_pool.empty()) {
+        hipEvent_t e = g_lprof_pool.back();
+        g_lprof_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
+
+// Events of one sampled step, or false when this step is not sampled (or an
+// event could not be created).  Caller holds plan->mu.
+bool lprof_begin(zero_lamb_plan* plan, LambProfRec* rec) {
+    const int every = prof_every();
+    if (every <= 0 || plan->prof_tick++ % (uint64_t)every != 0)
+        return false;
+    std::lock_guard<std::mutex> lk(g_lprof_mu);
+    bool ok = true;
+    for (int i = 0; i < 5; ++i) {
+        rec->e[i] = lprof_event();
+        ok = ok && rec->e[i];
+    }
+    if (!ok) {
+        for (int i = 0; i < 5; ++i)
+            if (rec->e[i])
+                g_lprof_pool.push_back(rec->e[i]);
+        return false;
+    }
+    return true;
+}
+
+int lprof_drain_locked() {
+    for (LambProfRec& r : g_lprof_pending) {
+        HIP_TRY(hipEventSynchronize(r.e[4]));
+        float t[4];
+        for (int i = 0; i < 4; ++i)
+            HIP_TRY(hipEventElapsedTime(&t[i], r.e[i], r.e[i + 1]));
+        g_lprof_acc.steps += 1;
+        g_lprof_acc.stats_ms += t[0];
+        g_lprof_acc.moments_ms += t[1];
+        g_lprof_acc.layer_ms += t[2];
+        g_lprof_acc.apply_ms += t[3];
+    }
+    for (LambProfRec& r : g_lprof_pending)
+        for (int i = 0; i < 5; ++i)
+            g_lprof_pool.push_back(r.e[i]);
+    g_lprof_pending.clear();
+    return ZERO_OK;
+}
+
+void set_last_stats(const zs::Result& r, int64_t n) {
+    t_stats.sumsq = r.sumsq;
+    t_stats.norm = r.norm;
+    t_stats.coef = r.coef;
+    t_stats.mult = r.mult;
+    t_stats.overflow = r.overflow;
+    t_stats.skipped = r.skip;
+    t_stats.pad_ = 0;
+    t_stats.n = n;
+    t_have_stats = true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int zero_lamb_plan_create(const int64_t* seg_off, int32_t n_seg, int64_t n, zero_lamb_plan_t** out) {
+    if (!out)
+        return fail(ZERO_EINVAL, "zero_lamb_plan_create: NULL out");
+    *out = nullptr;
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "zero_lamb_plan_create: n=%lld outside [0, 2^40]", (long long)n);
+    if (n_seg < 0 || (n == 0) != (n_seg == 0))
+        return fail(ZERO_EINVAL, "zero_lamb_plan_create: need n_seg > 0 for n > 0 and n_seg = 0 for n = 0");
+    if (n_seg > 0) {
+        if (!seg_off)
+            return fail(ZERO_EINVAL, "zero_lamb_plan_create: NULL seg_off");
+        if (seg_off[0] != 0 || seg_off[n_seg] != n)
+            return fail(ZERO_EINVAL, "zero_lamb_plan_create: seg_off must start at 0 and end at n");
+        for (int32_t s = 0; s < n_seg; ++s)
+            if (seg_off[s + 1] <= seg_off[s])
+                return fail(ZERO_EINVAL, "zero_lamb_plan_create: seg_off must rise strictly (layer %d)", s);
+    }
+    std::unique_ptr<zero_lamb_plan> p(new zero_lamb_plan);
+    HIP_TRY(hipGetDevice(&p->dev));
+    p->n = n;
+    p->n_seg = n_seg;
+    if (n_seg > 0)
+        p->seg_off.assign(seg_off, seg_off + n_seg + 1);
+    else
+        p->seg_off.assign(1, 0);
+    p->max_items = max_items_for(n, n_seg);
+    if (n > 0) {
+        if (hipMalloc(reinterpret_cast<void**>(&p->part), (size_t)p->max_items * sizeof(zs::LayerSums)) !=
+                hipSuccess ||
+            hipMalloc(reinterpret_cast<void**>(&p->sums), (size_t)n_seg * sizeof(zs::LayerSums)) != hipSuccess) {
+            if (p->part) (void)hipFree(p->part);
+            (void)hipGetLastError();
+            return fail(ZERO_ENOMEM, "zero_lamb_plan_create: could not allocate the plan workspace");
+        }
+        hipDeviceProp_t prop;
+        HIP_TRY(hipGetDeviceProperties(&prop, p->dev));
+        int resident = 0;
+        p->lds[0] = occupancy_lds(moments_kernel<true>(), kLambBlock, kLambPerCU, prop, &resident);
+        p->lds[1] = occupancy_lds(apply_kernel<true>(), kLambBlock, kLambPerCU, prop, &resident);
+        p->lds_scalar[0] = occupancy_lds(moments_kernel<false>(), kLambBlock, kLambPerCU, prop, &resident);
+        p->lds_scalar[1] = occupancy_lds(apply_kernel<false>(), kLambBlock, kLambPerCU, prop, &resident);
+    }
+    *out = p.release();
+    return ZERO_OK;
+}
+
+int zero_lamb_plan_destroy(zero_lamb_plan_t* plan) {
+    if (!plan)
+        return ZERO_OK;
+    int rc = ZERO_OK;
+    {
+        std::lock_guard<std::mutex> lk(plan->mu);
+        int cur = 0;
+        if (hipGetDevice(&cur) == hipSuccess && cur != plan->dev)
+            (void)hipSetDevice(plan->dev);
+        if (hipDeviceSynchronize() != hipSuccess)
+            rc = fail(ZERO_EHIP, "zero_lamb_plan_destroy: device synchronisation failed");
+        for (LambWork& w : plan->work) {
+            if (w.items) (void)hipFree(w.items);
+            if (w.first) (void)hipFree(w.first);
+        }
+        if (plan->part) (void)hipFree(plan->part);
+        if (plan->sums) (void)hipFree(plan->sums);
+        if (cur != plan->dev)
+            (void)hipSetDevice(cur);
+    }
+    delete plan;
+    return rc;
+}
+
+int zero_lamb_step(const zero_lamb_plan_t* plan_, const uint16_t* grad16, float* master32, float* m32, float* v32,
+                   uint16_t* param16_out, double lr, double beta1, double beta2, double eps, double weight_decay,
+                   int64_t step, double loss_scale, double clip, double phi_lo, double phi_hi, void* stream_) {
+    const char* fn = "zero_lamb_step";
+    zero_lamb_plan* plan = const_cast<zero_lamb_plan*>(plan_);
+    int rc = check_plan(fn, plan);
+    if (rc || (rc = check_hyper(fn, lr, beta1, beta2, eps, weight_decay, step, loss_scale, clip)) ||
+        (rc = check_phi(fn, phi_lo, phi_hi)))
+        return rc;
+    const int64_t n = plan->n;
+    if (n > 0 && (!grad16 || !master32 || !m32 || !v32 || !param16_out))
+        return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
+    const void* arrays[5] = {grad16, master32, m32, v32, param16_out};
+    if ((rc = check_lamb_arrays(fn, arrays, n)))
+        return rc;
+    if (n == 0) {
+        t_stats = zero_step_stats_t{0.0, 0.0, 1.0, (float)(1.0 / loss_scale), 0, 0, 0, 0};
+        t_have_stats = true;
+        return ZERO_OK;
+    }
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> plk(plan->mu);
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    const int phase = phase_of(grad16, master32, m32, v32, param16_out);
+    LambWork* w = nullptr;
+    if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
+        return rc;
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
+    const uint32_t seq = next_seq(ctx);
+    LambProfRec pr;
+    const bool prof = lprof_begin(plan, &pr);
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[0], stream));
+    if ((rc = launch_stats_planned(ctx, grad16, n, loss_scale, clip, seq, stream)))
+        return rc;
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[1], stream));
+    if ((rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream)))
+        return rc;
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[2], stream));
+    if ((rc = launch_layer(plan, *w, plan->sums, ctx->res, stream)))
+        return rc;
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.e[3], stream));
+    if ((rc = launch_apply(plan, *w, phase, master32, m32, v32, param16_out, plan->sums, ctx->res, c, lr, phi_lo,
+                           phi_hi, stream)))
+        return rc;
+    if (prof) {
+        HIP_TRY(hipEventRecord(pr.e[4], stream));
+        std::lock_guard<std::mutex> lk2(g_lprof_mu);
+        g_lprof_pending.push_back(pr);
+        if (g_lprof_pending.size() >= 4096 && (rc = lprof_drain_locked()))
+            return rc;
+    }
+    zs::Result r;
+    if ((rc = wait_result(ctx, seq, stream, &r)))
+        return rc;
+    set_last_stats(r, n);
+    return r.skip ? ZERO_SKIPPED : ZERO_OK;
+}
+
+int zero_lamb_moments(const zero_lamb_plan_t* plan_, const uint16_t* grad16, const float* master32, float* m32,
+                      float* v32, double global_sumsq, double beta1, double beta2, double eps, double weight_decay,
+                      int64_t step, double loss_scale, double clip, double* layer_sumsq, void* stream_) {
+    const char* fn = "zero_lamb_moments";
+    zero_lamb_plan* plan = const_cast<zero_lamb_plan*>(plan_);
+    int rc = check_plan(fn, plan);
+    if (rc || (rc = check_hyper(fn, 0.0, beta1, beta2, eps, weight_decay, step, loss_scale, clip)))
+        return rc;
+    if (std::isnan(global_sumsq) || global_sumsq < 0.0)
+        return fail(ZERO_EINVAL, "%s: global_sumsq must be >= 0 (+inf for an overflow)", fn);
+    const int64_t n = plan->n;
+    if (n > 0 && (!grad16 || !master32 || !m32 || !v32))
+        return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
+    const void* arrays[5] = {grad16, master32, m32, v32, nullptr};
+    if ((rc = check_lamb_arrays(fn, arrays, n)))
+        return rc;
+    if (n > 0 && (rc = check_layer_sums(fn, plan, layer_sumsq, arrays)))
+        return rc;
+    if (!std::isfinite(global_sumsq))
+        return ZERO_SKIPPED;
+    if (n == 0)
+        return ZERO_OK;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> plk(plan->mu);
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    const int phase = phase_of(grad16, master32, m32, v32, nullptr);
+    LambWork* w = nullptr;
+    if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
+        return rc;
+    const zs::AdamConst c = adam_const(0.0, beta1, beta2, eps, weight_decay, step);
+    const uint32_t seq = next_seq(ctx);
+    zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
+    HIP_TRY(hipGetLastError());
+    if ((rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream)))
+        return rc;
+    return launch_layer(plan, *w, reinterpret_cast<zs::LayerSums*>(layer_sumsq), ctx->res, stream);
+}
+
+int zero_lamb_apply(const zero_lamb_plan_t* plan_, float* master32, const float* m32, const float* v32,
+                    uint16_t* param16_out, double global_sumsq, const double* layer_sumsq, double lr, double beta1,
+                    double beta2, double eps, double weight_decay, int64_t step, double phi_lo, double phi_hi,
+                    void* stream_) {
+    const char* fn = "zero_lamb_apply";
+    zero_lamb_plan* plan = const_cast<zero_lamb_plan*>(plan_);
+    int rc = check_plan(fn, plan);
+    if (rc || (rc = check_hyper(fn, lr, beta1, beta2, eps, weight_decay, step, 1.0, 0.0)) ||
+        (rc = check_phi(fn, phi_lo, phi_hi)))
+        return rc;
+    if (std::isnan(global_sumsq) || global_sumsq < 0.0)
+        return fail(ZERO_EINVAL, "%s: global_sumsq must be >= 0 (+inf for an overflow)", fn);
+    const int64_t n = plan->n;
+    if (n > 0 && (!master32 || !m32 || !v32 || !param16_out))
+        return fail(ZERO_EINVAL, "%s: NULL array with n > 0", fn);
+    const void* arrays[5] = {nullptr, master32, m32, v32, param16_out};
+    if ((rc = check_lamb_arrays(fn, arrays, n)))
+        return rc;
+    if (n > 0 && (rc = check_layer_sums(fn, plan, layer_sumsq, arrays)))
+        return rc;
+    if (!std::isfinite(global_sumsq))
+        return ZERO_SKIPPED;
+    if (n == 0)
+        return ZERO_OK;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> plk(plan->mu);
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    const int phase = phase_of(nullptr, master32, m32, v32, param16_out);
+    LambWork* w = nullptr;
+    if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
+        return rc;
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
+    const uint32_t seq = next_seq(ctx);
+    // the apply kernel reads only the skip flag of the record: not skipped here
+    zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, 0.0, 1.0, 0.0, seq);
+    HIP_TRY(hipGetLastError());
+    return launch_apply(plan, *w, phase, master32, m32, v32, param16_out,
+                        reinterpret_cast<const zs::LayerSums*>(layer_sumsq), ctx->res, c, lr, phi_lo, phi_hi, stream);
+}
+
+int zero_lamb_profile_read(zero_lamb_profile_t* out) {
+    if (!out)
+        return fail(ZERO_EINVAL, "zero_lamb_profile_read: NULL out");
+    std::lock_guard<std::mutex> lk(g_lprof_mu);
+    int rc = lprof_drain_locked();
+    if (rc)
+        return rc;
+    *out = g_lprof_acc;
+    g_lprof_acc = zero_lamb_profile_t{0, 0.0, 0.0, 0.0, 0.0};
+    return ZERO_OK;
+}
+
+}  // extern "C"

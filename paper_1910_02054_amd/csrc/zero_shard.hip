@@ -22,8 +22,9 @@
 
 #include "zero_shard.h"
 #include "shard_kernels.hpp"
+#include "host_common.hpp"
 
-namespace {
+namespace zsh {
 
 thread_local std::string t_err;
 thread_local zero_step_stats_t t_stats;
@@ -38,13 +39,6 @@ int fail(int code, const char* fmt, ...) {
     t_err = buf;
     return code;
 }
-
-#define HIP_TRY(expr)                                                                        \
-    do {                                                                                     \
-        hipError_t e_ = (expr);                                                              \
-        if (e_ != hipSuccess)                                                                \
-            return fail(ZERO_EHIP, "%s: %s", #expr, hipGetErrorString(e_));                  \
-    } while (0)
 
 // ---------------------------------------------------------------------------
 // Production launch policy of the streaming kernels (template knobs in
@@ -142,22 +136,8 @@ size_t occupancy_lds(const void* kernel, int block, int per_cu, const hipDeviceP
 }
 
 // ---------------------------------------------------------------------------
-// Per-(device, stream) context: the constant-size workspace.
+// Per-(device, stream) context (struct Ctx in host_common.hpp).
 // ---------------------------------------------------------------------------
-struct Ctx {
-    std::mutex mu;
-    zs::Partial* part = nullptr;    // kMaxStatsBlocks partial records (device)
-    zs::Result* res = nullptr;      // result record (device), read by the update kernel
-    zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
-    zs::Result* host_dev = nullptr; // its device-side address
-    hipEvent_t prof_last_end = nullptr;  // end event of the last profiled update on this stream
-    uint64_t prof_tick = 0;              // steps seen while profiling (for sampling)
-    uint32_t seq = 0;               // call counter echoed in the result record
-    int ncu = 0;
-    size_t stats_lds = 0, adam_lds = 0;   // occupancy reservations (dynamic LDS per workgroup)
-    int stats_resident = 0, adam_resident = 0;
-    uintptr_t checked[6] = {0, 0, 0, 0, 0, 0};  // last (arrays, n) whose ranges were verified
-};
 
 std::mutex g_ctx_mu;
 std::map<std::pair<int, hipStream_t>, std::unique_ptr<Ctx>> g_ctx;
@@ -267,8 +247,6 @@ bool is_fin(double x) { return std::isfinite(x); }
 
 bool overlaps(uintptr_t a, size_t an, uintptr_t b, size_t bn) { return a < b + bn && b < a + an; }
 
-constexpr int64_t kMaxNumel = (int64_t)1 << 40;
-
 // Call sequence numbers skip 0: the finalize kernel writes the host record with
 // sequence number 0 before publishing the real one.
 uint32_t next_seq(Ctx* ctx) {
@@ -322,9 +300,8 @@ int check_arrays(const char* fn, const uint16_t* grad16, const float* master32, 
     return check_arrays_disjoint(fn, a, n);
 }
 
-int check_update_args(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
-                      const float* v32, const uint16_t* param16_out, int64_t n, double lr, double beta1,
-                      double beta2, double eps, double weight_decay, int64_t step, double loss_scale, double clip) {
+int check_hyper(const char* fn, double lr, double beta1, double beta2, double eps, double weight_decay, int64_t step,
+                double loss_scale, double clip) {
     if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
         return fail(ZERO_EINVAL, "%s: need finite lr >= 0, eps >= 0, weight_decay", fn);
     if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
@@ -335,7 +312,14 @@ int check_update_args(const char* fn, const uint16_t* grad16, const float* maste
         return fail(ZERO_EINVAL, "%s: loss_scale must be finite and > 0", fn);
     if (std::isnan(clip))
         return fail(ZERO_EINVAL, "%s: clip is NaN", fn);
-    return check_arrays(fn, grad16, master32, m32, v32, param16_out, n);
+    return ZERO_OK;
+}
+
+int check_update_args(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
+                      const float* v32, const uint16_t* param16_out, int64_t n, double lr, double beta1,
+                      double beta2, double eps, double weight_decay, int64_t step, double loss_scale, double clip) {
+    const int rc = check_hyper(fn, lr, beta1, beta2, eps, weight_decay, step, loss_scale, clip);
+    return rc ? rc : check_arrays(fn, grad16, master32, m32, v32, param16_out, n);
 }
 
 // Every array must lie inside one allocation the GPU can access: [p, p + bytes)
@@ -410,6 +394,17 @@ int launch_stats(Ctx* ctx, const uint16_t* grad16, int64_t n, const Plan& pl, do
     return ZERO_OK;
 }
 
+int launch_stats_planned(Ctx* ctx, const uint16_t* grad16, int64_t n, double loss_scale, double clip, uint32_t seq,
+                         hipStream_t stream) {
+    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
+    return launch_stats(ctx, grad16, n, pl, loss_scale, clip, seq, stream);
+}
+
+int prof_every() {
+    std::lock_guard<std::mutex> plk(g_prof_mu);
+    return g_prof_every;
+}
+
 // The fused update reading its scalars from ctx->res.
 int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
                   int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream) {
@@ -482,7 +477,9 @@ int prof_end(Ctx* ctx, const ProfRec& rec) {
     return ZERO_OK;
 }
 
-}  // namespace
+}  // namespace zsh
+
+using namespace zsh;
 
 // ===========================================================================
 // C ABI

@@ -178,3 +178,75 @@ def random_case(seed: int, n: int, grad_std: float = 1e-3, loss_scale: float = 2
     z = r.standard_normal(n, dtype=np.float32) * np.float32(grad_std * loss_scale)
     g16 = z.astype(np.float16).view(np.uint16).copy()
     return g16, master, m, v
+
+
+# ---------------------------------------------------------------------------
+# Layer structure (for the per-layer trust ratio of LAMB)
+# ---------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class ModelShape:
+    """A GPT-2-like transformer as in ZeRO's evaluation (Sec. 10 and its
+    appendix tables), sliced for mp-way model parallelism the Megatron way:
+    the QKV and first MLP projections split by columns (weights and biases),
+    the attention output and second MLP projections by rows (weights split,
+    biases replicated), layer norms replicated, the token embedding split by
+    vocabulary rows."""
+    hidden: int
+    mp: int = 1
+    vocab: int = 50257
+    positions: int = 1024
+
+
+MODEL_SHAPES = {
+    "tiny": ModelShape(hidden=128, vocab=2048, positions=256),
+    "gpt2_1p5b": ModelShape(hidden=1600),             # 48 layers, HD 1600, MP 1
+    "dp_13b": ModelShape(hidden=4096),                # the 10B-13B points: HD 4096, MP 1
+    "mp16_dp25_100b": ModelShape(hidden=8192, mp=16),  # 125 layers, HD 8192, MP 16
+    "ragged_1t": ModelShape(hidden=25600, mp=16),     # no shape in the paper: HD 25600 gives ~1T
+}
+
+
+def _layer_tensors(s: ModelShape):
+    h, mp = s.hidden, s.mp
+    return [h, h,                         # attention layer norm
+            h * (3 * h // mp), 3 * h // mp,  # QKV (column-parallel)
+            (h // mp) * h, h,             # attention output (row-parallel; bias replicated)
+            h, h,                         # MLP layer norm
+            h * (4 * h // mp), 4 * h // mp,  # MLP up (column-parallel)
+            (4 * h // mp) * h, h]         # MLP down (row-parallel; bias replicated)
+
+
+def model_tensor_sizes(shape: ModelShape, psi: int):
+    """Sizes of the model slice's tensors in flat order (token and position
+    embeddings, then transformer layers as many as needed), the last one cut
+    so that the sizes add up to exactly psi."""
+    sizes = []
+    total = 0
+    emb = [-(-shape.vocab // shape.mp) * shape.hidden, shape.positions * shape.hidden]
+    layer = _layer_tensors(shape)
+    k = 0
+    while total < psi:
+        t = emb[k] if k < len(emb) else layer[(k - len(emb)) % len(layer)]
+        t = min(t, psi - total)
+        sizes.append(t)
+        total += t
+        k += 1
+    return sizes
+
+
+def layer_offsets_in(sizes, start: int, stop: int) -> np.ndarray:
+    """The layer table of the flat range [start, stop): offsets relative to
+    start of the pieces of every tensor that meets the range (n_seg + 1
+    entries, from 0 to stop - start).  Bookkeeping only."""
+    bounds = np.concatenate([[0], np.cumsum(np.asarray(sizes, dtype=np.int64))])
+    inner = bounds[(bounds > start) & (bounds < stop)]
+    return np.concatenate([[start], inner, [stop]]).astype(np.int64) - start
+
+
+def layer_ids_in(sizes, start: int, stop: int) -> np.ndarray:
+    """Global tensor index of each layer of layer_offsets_in(sizes, start, stop)."""
+    bounds = np.concatenate([[0], np.cumsum(np.asarray(sizes, dtype=np.int64))])
+    first = int(np.searchsorted(bounds, start, side="right")) - 1
+    n_seg = layer_offsets_in(sizes, start, stop).size - 1
+    return np.arange(first, first + n_seg, dtype=np.int64)

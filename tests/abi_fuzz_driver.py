@@ -59,4 +59,25 @@ for _ in range(2000):
     ptrs = [p + r.choice([0, 1, 2, 8]) for p in G]
     L.zero_shard_validate(*ptrs, r.choice([-1, 0, 10, 1 << 41]))
     L.zero_last_error()
+L.zero_lamb_plan_create.argtypes = [P, i32, i64, ctypes.POINTER(P)]
+L.zero_lamb_plan_destroy.argtypes = [P]
+L.zero_lamb_step.argtypes = [P, P, P, P, P, P, dbl, dbl, dbl, dbl, dbl, i64, dbl, dbl, dbl, dbl, P]
+L.zero_lamb_moments.argtypes = [P, P, P, P, P, dbl, dbl, dbl, dbl, dbl, i64, dbl, dbl, P, P]
+L.zero_lamb_apply.argtypes = [P, P, P, P, P, dbl, P, dbl, dbl, dbl, dbl, dbl, i64, dbl, dbl, P]
+plan = P()
+for _ in range(3000):
+    k = r.randrange(0, 6)
+    offs = sorted(r.randrange(-2, 50) for _ in range(k + 1))
+    if r.random() < 0.5 and offs:
+        offs[0] = 0
+    arr = (ctypes.c_int64 * max(1, len(offs)))(*offs) if offs else None
+    n = offs[-1] if offs and r.random() < 0.7 else r.randrange(-3, 60)
+    L.zero_lamb_plan_create(arr if r.random() < 0.95 else None, k, n, ctypes.byref(plan) if r.random() < 0.9 else None)
+    L.zero_last_error()
+L.zero_lamb_plan_destroy(None)
+for _ in range(500):
+    L.zero_lamb_step(None, *G, 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 65536.0, 1.0, 0.0, float("inf"), None)
+    L.zero_lamb_moments(None, *G[:4], 1.0, 0.9, 0.999, 1e-6, 0.0, 1, 65536.0, 1.0, G[4], None)
+    L.zero_lamb_apply(None, *G[1:], 1.0, G[0], 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 0.0, float("inf"), None)
+    L.zero_last_error()
 print("driver done", bad, "rejected or empty calls")

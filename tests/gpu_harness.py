@@ -55,6 +55,37 @@ def oracle_step(g16, theta, m, v, p16, lr, beta1, beta2, eps, wd, t, scale, clip
     return 0, sc
 
 
+def oracle_lamb_step(g16, theta, m, v, p16, seg_off, lr, beta1, beta2, eps, wd, t, scale, clip, phi_lo=0.0,
+                     phi_hi=float("inf"), global_sumsq_units=None):
+    """In-place oracle LAMB step over host arrays; returns (skip, Scalars, per-layer array).
+
+    The gradient statistics are exact per chunk (threads); the layers are then
+    updated one oracle call each, in threads (layers are independent given the
+    multiplier: pinned in tests/test_oracle_lamb.py).  global_sumsq_units
+    replaces the local statistics (the split-phase case: the sum over every
+    rank's gradient)."""
+    n = g16.size
+    if global_sumsq_units is None:
+        spans = [(a, min(n, a + _CHUNK)) for a in range(0, n, _CHUNK)]
+        parts = list(_POOL.map(lambda s: oracle.local_stats(g16[s[0]:s[1]]), spans))
+        total, ovf = sum(p[0] for p in parts), (1 if any(p[1] for p in parts) else 0)
+    else:
+        total, ovf = global_sumsq_units
+    sc = oracle.scalars(total, ovf, scale, clip)
+    if sc.skip:
+        return 1, sc, None
+    hp = oracle.hyper(lr, beta1, beta2, eps, wd, t)
+    off = np.asarray(seg_off, np.int64)
+
+    def run(k):
+        a, b = int(off[k]), int(off[k + 1])
+        return oracle.lamb(g16[a:b], theta[a:b], m[a:b], v[a:b], p16[a:b], np.array([0, b - a], np.int64),
+                           sc.mult, hp, lr, phi_lo, phi_hi)
+
+    outs = list(_POOL.map(run, range(off.size - 1)))
+    return 0, sc, np.concatenate(outs) if outs else np.zeros((0, 3))
+
+
 class Guarded:
     """A device buffer of n elements with GUARD canary elements on both sides
     (and optional extra leading elements to misalign the view)."""

@@ -183,3 +183,43 @@ def test_validate_rejects_without_launching(zb):
     # plausible addresses that are not GPU allocations (no GPU here at all): rejected
     assert lib.zero_shard_validate(*GOOD, 10) == zb.ZERO_EINVAL
     assert "GPU-accessible" in zb.zero_last_error()
+
+
+def test_lamb_plan_rejects_bad_tables_without_a_gpu(zb):
+    lib = zb.raw_library()
+    out = ctypes.c_void_p()
+
+    def create(offs, n_seg, n, with_out=True):
+        arr = (ctypes.c_int64 * len(offs))(*offs) if offs is not None else None
+        return lib.zero_lamb_plan_create(arr, n_seg, n, ctypes.byref(out) if with_out else None)
+
+    assert create([0, 5, 5, 10], 3, 10) == zb.ZERO_EINVAL      # not strictly rising
+    assert create([0, 6, 4, 10], 3, 10) == zb.ZERO_EINVAL
+    assert create([0, 5, 9], 2, 10) == zb.ZERO_EINVAL          # does not end at n
+    assert create([1, 5, 10], 2, 10) == zb.ZERO_EINVAL         # does not start at 0
+    assert create([0], 0, 10) == zb.ZERO_EINVAL                # n > 0 needs layers
+    assert create([0, 1], 1, 0) == zb.ZERO_EINVAL              # n = 0 needs none
+    assert create([0, 10], 1, -1) == zb.ZERO_EINVAL
+    assert create([0, (1 << 40) + 1], 1, (1 << 40) + 1) == zb.ZERO_EINVAL
+    assert create(None, 2, 10) == zb.ZERO_EINVAL
+    assert create([0, 10], 1, 10, with_out=False) == zb.ZERO_EINVAL
+    assert "seg_off" in zb.zero_last_error() or "out" in zb.zero_last_error()
+    # a valid table gets as far as asking for the device
+    assert create([0, 10], 1, 10) in (zb.ZERO_OK, zb.ZERO_EHIP)
+    if out.value:
+        assert lib.zero_lamb_plan_destroy(out) == zb.ZERO_OK
+    assert lib.zero_lamb_plan_destroy(None) == zb.ZERO_OK
+
+
+def test_lamb_calls_reject_a_null_plan(zb):
+    lib = zb.raw_library()
+    G = [0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000]
+    assert lib.zero_lamb_step(None, *G, 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 65536.0, 1.0, 0.0, float("inf"),
+                              None) == zb.ZERO_EINVAL
+    assert lib.zero_lamb_moments(None, *G[:4], 1.0, 0.9, 0.999, 1e-6, 0.0, 1, 65536.0, 1.0, G[4],
+                                 None) == zb.ZERO_EINVAL
+    assert lib.zero_lamb_apply(None, *G[1:], 1.0, G[0], 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 0.0, float("inf"),
+                               None) == zb.ZERO_EINVAL
+    assert "NULL plan" in zb.zero_last_error()
+    p = zb.LambProfile()
+    assert lib.zero_lamb_profile_read(ctypes.byref(p)) == zb.ZERO_OK and p.steps == 0
