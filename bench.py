@@ -11,7 +11,11 @@ kernel (the fused update, 28 bytes per parameter, timed with HIP events on its
 own stream inside the timed region), and the CPU oracle timed on a bounded
 sample of the same workload.
 
-    python bench.py [--steps K] [--warmup W] [--workload KEY] [--no-cpu-baseline]
+With --optimizer lamb the step is the LAMB shard step over the same shard and
+its GPT-2-like layer table (42 algorithmic bytes per parameter: statistics 2,
+moments pass 22, apply pass 18); the roofline is the moments pass's.
+
+    python bench.py [--steps K] [--warmup W] [--workload KEY] [--optimizer adam|lamb] [--no-cpu-baseline]
 """
 import argparse
 import hashlib
@@ -28,9 +32,15 @@ METRIC = "shard params updated/sec and achieved HBM GB/s (% of MI355X peak)"
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published
 STEP_BYTES_PER_PARAM = 30       # grad16 read twice (2+2), master/m/v read+write (24), p16 write (2)
 UPDATE_BYTES_PER_PARAM = 28     # the fused update kernel alone
+LAMB_STEP_BYTES_PER_PARAM = 42  # statistics 2, moments 14 read + 8 written, apply 12 read + 6 written
+LAMB_MOMENTS_BYTES_PER_PARAM = 22
+LAMB_APPLY_BYTES_PER_PARAM = 18
 DEFAULT_WORKLOAD = "mp16_dp25_100b"
+CSRC = os.path.join(ROOT, "paper_1910_02054_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_adam_vec_mp16_dp25_100b_traffic.txt")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_1910_02054_amd", "csrc", f) for f in ("shard_kernels.hpp", "zero_shard.hip")]
+LAMB_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lamb_moments_mp16_dp25_100b_traffic.txt")
+KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "zero_shard.hip")]
+LAMB_KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "lamb_kernels.hpp", "zero_lamb.hip")]
 
 
 def _code_only(text: str) -> str:
@@ -55,23 +65,48 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(n):
-    """HBM bytes per update launch from the committed counter summary, or None when
-    absent, for another shard size, or taken on a different kernel source."""
-    if not os.path.exists(TRAFFIC_FILE):
+def lamb_kernel_source_hash() -> str:
+    """Hash of the LAMB kernels' code (with the shared kernel header) and of their
+    launch policy (the constexpr block at the top of zero_lamb.hip)."""
+    h = hashlib.sha256()
+    for path in LAMB_KERNEL_SOURCES[:2]:
+        with open(path) as f:
+            h.update(_code_only(f.read()).encode())
+    with open(LAMB_KERNEL_SOURCES[2]) as f:
+        host = f.read()
+    a = host.index("constexpr int kLambBlock")
+    b = host.index("}  // namespace", a)
+    policy = [ln for ln in _code_only(host[a:b]).splitlines() if ln.startswith("constexpr")]
+    h.update("\n".join(policy).encode())
+    return h.hexdigest()[:16]
+
+
+def _traffic_from(path, key, source_hash, n):
+    if not os.path.exists(path):
         return None
     kv = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 kv[k.strip()] = v.strip()
     try:
-        if kv.get("kernel_source_sha256_16") != kernel_source_hash() or int(kv["shard_numel"]) != n:
+        if kv.get("kernel_source_sha256_16") != source_hash or int(kv["shard_numel"]) != n:
             return None
-        return float(kv["update_bytes_per_launch"])
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
+
+
+def measured_traffic(n):
+    """HBM bytes per update launch from the committed counter summary, or None when
+    absent, for another shard size, or taken on a different kernel source."""
+    return _traffic_from(TRAFFIC_FILE, "update_bytes_per_launch", kernel_source_hash(), n)
+
+
+def measured_lamb_traffic(n):
+    """HBM bytes per LAMB moments launch from the committed counter summary (same rules)."""
+    return _traffic_from(LAMB_TRAFFIC_FILE, "moments_bytes_per_launch", lamb_kernel_source_hash(), n)
 
 
 def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
@@ -97,6 +132,30 @@ def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
                       "update), single thread, %.1f s" % (done, n, t_used)}
 
 
+def lamb_cpu_baseline(w, seg, theta, m, v, g16, scale, budget_s):
+    """The oracle's LAMB step, as it stands, single-threaded on whole layers of the
+    shard in order (a layer's trust ratio needs all of it), until about budget_s
+    seconds of CPU time have been spent (wrapping around the shard)."""
+    import numpy as np
+    import oracle
+    done, t_used, k = 0, 0.0, 0
+    n_seg = seg.size - 1
+    while t_used < budget_s:
+        a, b = int(seg[k]), int(seg[k + 1])
+        th, mm, vv = theta[a:b].copy(), m[a:b].copy(), v[a:b].copy()
+        p16 = np.empty(b - a, np.uint16)
+        t0 = time.perf_counter()
+        oracle.lamb_step(g16[a:b], th, mm, vv, p16, [0, b - a], w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, 1,
+                         scale, w.clip)
+        t_used += time.perf_counter() - t0
+        done += b - a
+        k = (k + 1) % n_seg
+    return {"value": done / t_used, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": "%d element-updates over whole layers of the %d-element shard, one oracle LAMB step per "
+                      "layer (statistics + moments + exact layer norms + update), single thread, %.1f s"
+                      % (done, int(seg[-1]), t_used)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -109,6 +168,8 @@ def main():
                     help="time the kernels of one step in this many with HIP events (markers cost GPU time)")
     ap.add_argument("--probe-copy-mib", type=int, default=2048,
                     help="also run the library's copy kernel over this many MiB (counter calibration)")
+    ap.add_argument("--optimizer", choices=("adam", "lamb"), default="adam",
+                    help="adam: the mixed-precision Adam shard step; lamb: LAMB over the shard's layer table")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -143,11 +204,21 @@ def main():
     d_p = torch.empty(n, dtype=torch.float16, device=dev)
     stream = torch.cuda.current_stream()
     scaler = zb.Scaler(w.loss_scale)
+    lamb = args.optimizer == "lamb"
+    seg = plan = None
+    if lamb:
+        sizes = workloads.model_tensor_sizes(workloads.MODEL_SHAPES[w.key], w.psi)
+        seg = workloads.layer_offsets_in(sizes, lay.offset, lay.offset + n)
+        plan = zb.LambPlan(seg)
 
     def step():
         d_g = d_gs[scaler.t_next % 2]
-        flag = zb.zero_shard_step(d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
-                                  scaler.t_next, scaler.scale, w.clip, stream=stream)
+        if lamb:
+            flag = zb.zero_lamb_step(plan, d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps,
+                                     w.weight_decay, scaler.t_next, scaler.scale, w.clip, stream=stream)
+        else:
+            flag = zb.zero_shard_step(d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
+                                      scaler.t_next, scaler.scale, w.clip, stream=stream)
         scaler.update(flag)
         return flag
 
@@ -177,6 +248,7 @@ def main():
         step()
     torch.cuda.synchronize()
     zb.zero_profile_read()
+    zb.zero_lamb_profile_read()
     zb.zero_profile_enable(args.profile_every)
     skips = 0
     print("[bench] timing %d steps" % args.steps, file=sys.stderr, flush=True)
@@ -188,17 +260,27 @@ def main():
     t1 = time.perf_counter()
     zb.zero_profile_enable(False)
     prof = zb.zero_profile_read()
+    lprof = zb.zero_lamb_profile_read()
     if skips:
         print("bench.py: %d timed steps skipped on overflow; the measurement is invalid" % skips, file=sys.stderr)
         sys.exit(1)
 
     ms = (t1 - t0) * 1e3 / args.steps
     params_per_s = n / (ms * 1e-3)
-    step_gbps = STEP_BYTES_PER_PARAM * n / (ms * 1e-3) / 1e9
-    upd_ms = prof.update_ms / prof.steps
-    stats_ms = prof.stats_ms / prof.steps
-    upd_gbps = UPDATE_BYTES_PER_PARAM * n / (upd_ms * 1e-3) / 1e9
-    traffic = measured_traffic(n)
+    if lamb:
+        step_gbps = LAMB_STEP_BYTES_PER_PARAM * n / (ms * 1e-3) / 1e9
+        k = lprof.steps
+        kernel_ms = {"stats_and_finalize": lprof.stats_ms / k, "moments": lprof.moments_ms / k,
+                     "layer_sums": lprof.layer_ms / k, "apply": lprof.apply_ms / k, "profiled_steps": k}
+        upd_gbps = LAMB_MOMENTS_BYTES_PER_PARAM * n / (kernel_ms["moments"] * 1e-3) / 1e9
+        apply_gbps = LAMB_APPLY_BYTES_PER_PARAM * n / (kernel_ms["apply"] * 1e-3) / 1e9
+        roof_kernel, traffic = "k_lamb_moments", measured_lamb_traffic(n)
+    else:
+        step_gbps = STEP_BYTES_PER_PARAM * n / (ms * 1e-3) / 1e9
+        kernel_ms = {"stats_and_finalize": prof.stats_ms / prof.steps, "update": prof.update_ms / prof.steps,
+                     "profiled_steps": prof.steps}
+        upd_gbps = UPDATE_BYTES_PER_PARAM * n / (kernel_ms["update"] * 1e-3) / 1e9
+        roof_kernel, traffic = "k_adam_vec", measured_traffic(n)
 
     out = {
         "metric": METRIC,
@@ -217,17 +299,26 @@ def main():
                    "shard_numel": n, "parallelism": "one ZeRO P_os+g data-parallel rank (N_d=%d) per GPU" % w.nd},
         "hbm_gbps": step_gbps,
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
-        "kernel_ms": {"stats_and_finalize": stats_ms, "update": upd_ms, "profiled_steps": prof.steps},
-        "roofline": {"bound": "hbm", "kernel": "k_adam_vec", "achieved": upd_gbps, "peak": HBM_PEAK_GBPS,
+        "kernel_ms": kernel_ms,
+        "roofline": {"bound": "hbm", "kernel": roof_kernel, "achieved": upd_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
     }
+    if lamb:
+        out["config"].update(optimizer="lamb", layers=int(seg.size - 1))
+        out["lamb_apply"] = {"kernel": "k_lamb_apply", "achieved_gbps": apply_gbps,
+                             "frac": apply_gbps / HBM_PEAK_GBPS}
     if probe:
         probe["update_frac_of_copy"] = upd_gbps / probe["gbps"]
         out["copy_probe"] = probe
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, n, theta, m, v, g16, w.loss_scale, args.cpu_budget)
+        if lamb:
+            out["cpu_baseline"] = lamb_cpu_baseline(w, seg, theta, m, v, g16, w.loss_scale, args.cpu_budget)
+        else:
+            out["cpu_baseline"] = cpu_baseline(w, n, theta, m, v, g16, w.loss_scale, args.cpu_budget)
+    if plan is not None:
+        plan.close()
     print(json.dumps(out), flush=True)
 
 
