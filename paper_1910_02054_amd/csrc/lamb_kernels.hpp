@@ -8,13 +8,15 @@
 // streaming passes after the gradient statistics:
 //   k_lamb_moments  reads g16, theta, m, v; writes m, v; one fp64 partial
 //                   (sum theta^2, sum u^2) per work item (22 bytes/element).
-//   k_lamb_layer    fixed-order sum of each layer's partials.
+//   k_lamb_chunks,  fixed-order two-level sum of each layer's partials.
+//   k_lamb_layer
 //   k_lamb_apply    reads theta, m, v; recomputes u from the stored moments
 //                   (the same fp32 operations, so the same bits); writes
 //                   theta - step*u and its fp16 copy (18 bytes/element).
-// A work item is a run of at most one tile of elements inside one layer: the
-// host cuts the shard's tiles at the layer boundaries, so no workgroup needs a
-// segmented reduction and every item's partial belongs to one layer.
+// A work item is a tile's piece inside one layer: the host cuts the shard's
+// tiles at the layer boundaries.  Each workgroup owns one tile and computes its
+// addresses from its index alone; it reads the tile's items (almost always
+// one) only to attribute its partial sums and step sizes to layers.
 #pragma once
 
 #include "shard_kernels.hpp"
@@ -100,46 +102,63 @@ __device__ __forceinline__ void block_sum2(double& a, double& b) {
     }
 }
 
-// First element of the 4-element vector that holds element `start`, where
-// vectors begin at indices congruent to `head` mod 4 (head in 0..3; a start
-// below head lies in the partial vector that ends at head).
-__device__ __forceinline__ int64_t vec_floor(int64_t start, int64_t head) {
-    const int64_t d = start - head;
-    return head + 4 * (d >= 0 ? d / 4 : -1);
+// Tiles of the shard: with head h (0..3) the 4-element vectors begin at
+// indices congruent to h mod 4; tile 0 is [0, h) when h > 0, and the other
+// tiles are T = 4*BLOCK*U elements long, aligned to the vectors.  Returns the
+// first vector's element index (h - 4 for the partial tile [0, h)) and the
+// tile's element range [ts, te).
+template <int BLOCK, int U>
+__device__ __forceinline__ int64_t tile_range(int64_t b, int64_t head, int64_t n, int64_t* ts, int64_t* te) {
+    constexpr int64_t T = 4 * (int64_t)BLOCK * U;
+    const int64_t hs = head > 0 ? 1 : 0;
+    if (b < hs) {
+        *ts = 0;
+        *te = head < n ? head : n;
+        return head - 4;
+    }
+    const int64_t base = head + (b - hs) * T;
+    *ts = base;
+    *te = base + T < n ? base + T : n;
+    return base;
 }
 
 // ---------------------------------------------------------------------------
-// Moments pass.  Workgroup k handles item k (grid-strided): thread t covers the
-// U vectors base + 4*(t + u*BLOCK) .. +3, where base is the vector holding the
-// item's first element.  VEC: all arrays share the element misalignment
-// `head`, so a vector wholly inside the item is one 16-byte fp32 access per
-// array and one 8-byte fp16 access; elements of partial vectors (layer
-// boundaries, the array's ends) and every element when !VEC (head = 0) take
-// the scalar path.  Only elements of the item are read or written.
+// Moments pass.  Workgroup b (grid-strided over the tiles) owns tile b: thread
+// t covers the U vectors base + 4*(t + u*BLOCK) .. +3.  The data addresses
+// depend on b only, so the loads are issued before the tile's work items
+// (its layer pieces, [tile_first[b], tile_first[b+1]) of the item list) are
+// read; the items are needed only to attribute each element's theta^2 and u^2
+// to its layer piece.  VEC: all arrays share the element misalignment `head`,
+// so a vector inside the tile is one 16-byte fp32 access per array and one
+// 8-byte fp16 access; the partial vectors at the array's ends and every
+// element when !VEC (head = 0) take the scalar path.
 // ---------------------------------------------------------------------------
 template <int BLOCK, int U, bool NTL, bool NTS, bool VEC>
 __global__ __launch_bounds__(BLOCK) void k_lamb_moments(const uint16_t* __restrict__ g, const float* __restrict__ th,
                                                         float* __restrict__ m, float* __restrict__ v,
-                                                        const LambItem* __restrict__ items, int64_t n_items,
-                                                        int64_t head, const Result* __restrict__ res, AdamConst c,
-                                                        LayerSums* __restrict__ part) {
+                                                        const LambItem* __restrict__ items,
+                                                        const int64_t* __restrict__ tile_first, int64_t ntiles,
+                                                        int64_t n, int64_t head, const Result* __restrict__ res,
+                                                        AdamConst c, LayerSums* __restrict__ part) {
     if (res->skip)
         return;
     const float mult = res->mult;
-    for (int64_t k = blockIdx.x; k < n_items; k += gridDim.x) {
-        const int64_t start = items[k].start, end = items[k + 1].start;
-        const int64_t base = vec_floor(start, head);
-        double aw = 0.0, au = 0.0;
+    for (int64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+        int64_t ts, te;
+        const int64_t base = tile_range<BLOCK, U>(b, head, n, &ts, &te);
+        double w2[U][4], u2[U][4];
+        int64_t e0s[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t e0 = base + 4 * ((int64_t)threadIdx.x + (int64_t)u * BLOCK);
-            if (VEC && e0 >= start && e0 + 4 <= end) {
+            e0s[u] = e0;
+            if (VEC && e0 >= ts && e0 + 4 <= te) {
                 const u32x2 gq = ld<NTL>(reinterpret_cast<const u32x2*>(g + e0));
                 const f32x4 tq = ld<NTL>(reinterpret_cast<const f32x4*>(th + e0));
                 f32x4 mq = ld<NTL>(reinterpret_cast<const f32x4*>(m + e0));
                 f32x4 vq = ld<NTL>(reinterpret_cast<const f32x4*>(v + e0));
                 const uint32_t gw[4] = {gq.x & 0xFFFFu, gq.x >> 16, gq.y & 0xFFFFu, gq.y >> 16};
-                float t4[4] = {tq.x, tq.y, tq.z, tq.w};
+                const float t4[4] = {tq.x, tq.y, tq.z, tq.w};
                 float m4[4] = {mq.x, mq.y, mq.z, mq.w};
                 float v4[4] = {vq.x, vq.y, vq.z, vq.w};
 #pragma unroll
@@ -147,8 +166,8 @@ __global__ __launch_bounds__(BLOCK) void k_lamb_moments(const uint16_t* __restri
                     lamb_moments_elem(gw[j], mult, m4[j], v4[j], c);
                     const double ud = (double)lamb_dir(m4[j], v4[j], t4[j], c);
                     const double td = (double)t4[j];
-                    aw = __builtin_fma(td, td, aw);
-                    au = __builtin_fma(ud, ud, au);
+                    w2[u][j] = td * td;
+                    u2[u][j] = ud * ud;
                 }
                 st<NTS>(f32x4{m4[0], m4[1], m4[2], m4[3]}, reinterpret_cast<f32x4*>(m + e0));
                 st<NTS>(f32x4{v4[0], v4[1], v4[2], v4[3]}, reinterpret_cast<f32x4*>(v + e0));
@@ -156,44 +175,85 @@ __global__ __launch_bounds__(BLOCK) void k_lamb_moments(const uint16_t* __restri
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int64_t i = e0 + j;
-                    if (i >= start && i < end) {
+                    w2[u][j] = 0.0;
+                    u2[u][j] = 0.0;
+                    if (i >= ts && i < te) {
                         float mm = m[i], vv = v[i];
                         const float t = th[i];
                         lamb_moments_elem(g[i], mult, mm, vv, c);
                         const double ud = (double)lamb_dir(mm, vv, t, c);
                         const double td = (double)t;
-                        aw = __builtin_fma(td, td, aw);
-                        au = __builtin_fma(ud, ud, au);
+                        w2[u][j] = td * td;
+                        u2[u][j] = ud * ud;
                         m[i] = mm;
                         v[i] = vv;
                     }
                 }
             }
         }
-        block_sum2<BLOCK>(aw, au);
-        if (threadIdx.x == 0)
-            part[k] = LayerSums{aw, au};
+        // one partial per layer piece of the tile (almost always one piece)
+        const int64_t f = tile_first[b], l = tile_first[b + 1];
+        for (int64_t k = f; k < l; ++k) {
+            const int64_t s0 = items[k].start, s1 = items[k + 1].start;
+            double aw = 0.0, au = 0.0;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t i = e0s[u] + j;
+                    if (i >= s0 && i < s1) {
+                        aw += w2[u][j];
+                        au += u2[u][j];
+                    }
+                }
+            block_sum2<BLOCK>(aw, au);
+            if (threadIdx.x == 0)
+                part[k] = LayerSums{aw, au};
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
-// Layer sums: workgroup s adds the partials of layer s's items
-// [first[s], first[s+1]) in a fixed order (strided per thread, then the
-// workgroup tree), so the result is reproducible for a given item list.
+// Layer sums, two levels in a fixed order.  Level 1: workgroup c adds the
+// partials of item chunk c, items [chunk[c], chunk[c+1]) (a chunk never
+// spans two layers).  Level 2: workgroup s adds the chunk sums of layer s,
+// chunks [chunk_first[s], chunk_first[s+1]).
 // ---------------------------------------------------------------------------
-constexpr int kLayerBlock = 256;
+constexpr int kChunkBlock = 256;
+constexpr int kChunkItems = 1024;   // items per level-1 chunk (4 per thread)
+constexpr int kLayerBlock = 64;
 
-__global__ __launch_bounds__(kLayerBlock) void k_lamb_layer(const LayerSums* __restrict__ part,
-                                                            const int64_t* __restrict__ first, int64_t n_layers,
-                                                            LayerSums* __restrict__ sums,
+__global__ __launch_bounds__(kChunkBlock) void k_lamb_chunks(const LayerSums* __restrict__ part,
+                                                             const int64_t* __restrict__ chunk, int64_t n_chunks,
+                                                             LayerSums* __restrict__ cpart,
+                                                             const Result* __restrict__ res) {
+    if (res->skip)
+        return;
+    for (int64_t cb = blockIdx.x; cb < n_chunks; cb += gridDim.x) {
+        const int64_t a = chunk[cb], e = chunk[cb + 1];
+        double w = 0.0, u = 0.0;
+        for (int64_t i = a + threadIdx.x; i < e; i += kChunkBlock) {
+            const LayerSums p = part[i];
+            w += p.wsq;
+            u += p.usq;
+        }
+        block_sum2<kChunkBlock>(w, u);
+        if (threadIdx.x == 0)
+            cpart[cb] = LayerSums{w, u};
+    }
+}
+
+__global__ __launch_bounds__(kLayerBlock) void k_lamb_layer(const LayerSums* __restrict__ cpart,
+                                                            const int64_t* __restrict__ chunk_first,
+                                                            int64_t n_layers, LayerSums* __restrict__ sums,
                                                             const Result* __restrict__ res) {
     if (res->skip)
         return;
     for (int64_t s = blockIdx.x; s < n_layers; s += gridDim.x) {
-        const int64_t a = first[s], b = first[s + 1];
+        const int64_t a = chunk_first[s], e = chunk_first[s + 1];
         double w = 0.0, u = 0.0;
-        for (int64_t i = a + threadIdx.x; i < b; i += kLayerBlock) {
-            const LayerSums p = part[i];
+        for (int64_t i = a + threadIdx.x; i < e; i += kLayerBlock) {
+            const LayerSums p = cpart[i];
             w += p.wsq;
             u += p.usq;
         }
@@ -204,52 +264,98 @@ __global__ __launch_bounds__(kLayerBlock) void k_lamb_layer(const LayerSums* __r
 }
 
 // ---------------------------------------------------------------------------
-// Apply pass: same item walk as the moments pass; theta <- theta - step*u with
-// the item's layer step size, and the fp16 copy.
+// Apply pass: same tile walk as the moments pass; each element moves by its
+// layer piece's step size (theta <- theta - step*u) and gets its fp16 copy.
 // ---------------------------------------------------------------------------
 template <int BLOCK, int U, bool NTL, bool NTS, bool VEC>
 __global__ __launch_bounds__(BLOCK) void k_lamb_apply(float* __restrict__ th, const float* __restrict__ m,
                                                       const float* __restrict__ v, uint16_t* __restrict__ p,
-                                                      const LambItem* __restrict__ items, int64_t n_items,
-                                                      int64_t head, const LayerSums* __restrict__ sums,
+                                                      const LambItem* __restrict__ items,
+                                                      const int64_t* __restrict__ tile_first, int64_t ntiles,
+                                                      int64_t n, int64_t head, const LayerSums* __restrict__ sums,
                                                       const Result* __restrict__ res, AdamConst c, double lr,
                                                       double phi_lo, double phi_hi) {
 #pragma clang fp contract(off)
     if (res->skip)
         return;
-    for (int64_t k = blockIdx.x; k < n_items; k += gridDim.x) {
-        const LambItem it = items[k];
-        const int64_t start = it.start, end = items[k + 1].start;
-        const float step = lamb_step_size(sums[it.layer], lr, phi_lo, phi_hi);
-        const int64_t base = vec_floor(start, head);
+    for (int64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+        int64_t ts, te;
+        const int64_t base = tile_range<BLOCK, U>(b, head, n, &ts, &te);
+        float t4[U][4], u4[U][4];
+        bool full[U];
+        int64_t e0s[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int64_t e0 = base + 4 * ((int64_t)threadIdx.x + (int64_t)u * BLOCK);
-            if (VEC && e0 >= start && e0 + 4 <= end) {
+            e0s[u] = e0;
+            full[u] = VEC && e0 >= ts && e0 + 4 <= te;
+            if (full[u]) {
                 const f32x4 tq = ld<NTL>(reinterpret_cast<const f32x4*>(th + e0));
                 const f32x4 mq = ld<NTL>(reinterpret_cast<const f32x4*>(m + e0));
                 const f32x4 vq = ld<NTL>(reinterpret_cast<const f32x4*>(v + e0));
-                const float t4[4] = {tq.x, tq.y, tq.z, tq.w};
-                const float m4[4] = {mq.x, mq.y, mq.z, mq.w};
-                const float v4[4] = {vq.x, vq.y, vq.z, vq.w};
-                float o[4];
-                uint32_t h[4];
+                const float tt[4] = {tq.x, tq.y, tq.z, tq.w};
+                const float mm[4] = {mq.x, mq.y, mq.z, mq.w};
+                const float vv[4] = {vq.x, vq.y, vq.z, vq.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    o[j] = t4[j] - step * lamb_dir(m4[j], v4[j], t4[j], c);
-                    h[j] = f32_to_f16(o[j]);
+                    t4[u][j] = tt[j];
+                    u4[u][j] = lamb_dir(mm[j], vv[j], tt[j], c);
                 }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t i = e0 + j;
+                    t4[u][j] = 0.0f;
+                    u4[u][j] = 0.0f;
+                    if (i >= ts && i < te) {
+                        t4[u][j] = th[i];
+                        u4[u][j] = lamb_dir(m[i], v[i], t4[u][j], c);
+                    }
+                }
+            }
+        }
+        // the step size of every element's layer piece (almost always one piece per tile)
+        float step[U][4];
+        const int64_t f = tile_first[b], l = tile_first[b + 1];
+        {
+            const LambItem it = items[f];
+            const float s = lamb_step_size(sums[it.layer], lr, phi_lo, phi_hi);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    step[u][j] = s;
+        }
+        for (int64_t k = f + 1; k < l; ++k) {
+            const LambItem it = items[k];
+            const float s = lamb_step_size(sums[it.layer], lr, phi_lo, phi_hi);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (e0s[u] + j >= it.start)
+                        step[u][j] = s;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e0 = e0s[u];
+            float o[4];
+            uint32_t h[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                o[j] = t4[u][j] - step[u][j] * u4[u][j];
+                h[j] = f32_to_f16(o[j]);
+            }
+            if (full[u]) {
                 st<NTS>(f32x4{o[0], o[1], o[2], o[3]}, reinterpret_cast<f32x4*>(th + e0));
                 st<NTS>(u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, reinterpret_cast<u32x2*>(p + e0));
             } else {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int64_t i = e0 + j;
-                    if (i >= start && i < end) {
-                        const float t = th[i];
-                        const float o = t - step * lamb_dir(m[i], v[i], t, c);
-                        th[i] = o;
-                        p[i] = (uint16_t)f32_to_f16(o);
+                    if (i >= ts && i < te) {
+                        th[i] = o[j];
+                        p[i] = (uint16_t)h[j];
                     }
                 }
             }

@@ -20,11 +20,15 @@
 
 // ---------------------------------------------------------------------------
 // Launch policy of the two LAMB streaming passes (template knobs in
-// lamb_kernels.hpp): one tile of BLOCK*U 4-element vectors per work item, at
-// most kLambPerCU resident workgroups per CU (an LDS reservation).
+// lamb_kernels.hpp): one tile of BLOCK*U 4-element vectors per workgroup, at
+// most kLambPerCU resident workgroups per CU (an LDS reservation).  Measured on
+// MI355X over 250M-element shards: both passes run best with about 32 resident
+// waves per CU (128 threads x 16 workgroups, one vector per thread), unlike
+// the Adam update, whose optimum is 12 single-wave workgroups; each workgroup
+// here also reads its tile's layer pieces and reduces a partial sum.
 // ---------------------------------------------------------------------------
 namespace {
-constexpr int kLambBlock = 64, kLambUnroll = 1, kLambPerCU = 12;
+constexpr int kLambBlock = 128, kLambUnroll = 1, kLambPerCU = 16;
 constexpr bool kLambNTL = true, kLambNTS = true;
 constexpr int64_t kLambTile = 4 * (int64_t)kLambBlock * kLambUnroll;  // elements per tile
 constexpr int64_t kLambMaxBlocks = 1 << 26;
@@ -33,12 +37,16 @@ constexpr int kPhases = 5;  // vector paths for element misalignment 0..3, then 
 
 using namespace zsh;
 
-// The work list of one array alignment: items (with the end sentinel) and the
-// first item of every layer (with the end sentinel), on the device.
+// The work lists of one array alignment, on the device: the items (tile pieces
+// inside one layer, with the end sentinel), the first item of every tile, the
+// level-1 chunks of the layer sums (item ranges inside one layer) and the first
+// chunk of every layer (each list with its end sentinel).
 struct LambWork {
     zs::LambItem* items = nullptr;
-    int64_t* first = nullptr;
-    int64_t n_items = 0;
+    int64_t* tile_first = nullptr;
+    int64_t* chunk = nullptr;
+    int64_t* chunk_first = nullptr;
+    int64_t n_items = 0, ntiles = 0, n_chunks = 0;
     bool built = false;
 };
 
@@ -53,9 +61,10 @@ struct zero_lamb_plan {
     int32_t n_seg = 0;
     std::vector<int64_t> seg_off;
     LambWork work[kPhases];
-    zs::LayerSums* part = nullptr;  // one partial per item (sized for the longest list)
-    zs::LayerSums* sums = nullptr;  // per-layer sums of zero_lamb_step
-    int64_t max_items = 0;
+    zs::LayerSums* part = nullptr;   // one partial per item (sized for the longest list)
+    zs::LayerSums* cpart = nullptr;  // one partial per level-1 chunk
+    zs::LayerSums* sums = nullptr;   // per-layer sums of zero_lamb_step
+    int64_t max_items = 0, max_chunks = 0;
     hipStream_t last_stream = nullptr;
     bool used = false;
     uint64_t prof_tick = 0;
@@ -84,28 +93,77 @@ const void* apply_kernel() {
 // plus one per interior layer boundary.
 int64_t max_items_for(int64_t n, int32_t n_seg) { return n / kLambTile + 2 + (int64_t)n_seg; }
 
-// Cut [0, n) at tile boundaries (head + k*T, plus 0) and at layer boundaries.
-void build_items(const std::vector<int64_t>& off, int32_t n_seg, int64_t head, std::vector<zs::LambItem>* items,
-                 std::vector<int64_t>* first) {
-    items->clear();
-    first->assign((size_t)n_seg + 1, 0);
+// Level-1 chunks: each layer's items cut into runs of at most kChunkItems.
+int64_t max_chunks_for(int64_t max_items, int32_t n_seg) { return max_items / zs::kChunkItems + 1 + (int64_t)n_seg; }
+
+// Tiles (as the kernels' tile_range defines them): [0, head) when head > 0,
+// then runs of kLambTile elements from head on.
+int64_t tile_of(int64_t pos, int64_t head) {
+    const int64_t hs = head > 0 ? 1 : 0;
+    return pos < head ? 0 : hs + (pos - head) / kLambTile;
+}
+
+int64_t tile_count(int64_t n, int64_t head) {
+    if (n == 0)
+        return 0;
+    const int64_t hs = head > 0 ? 1 : 0;
+    return n > head ? hs + (n - head + kLambTile - 1) / kLambTile : 1;
+}
+
+struct HostWork {
+    std::vector<zs::LambItem> items;  // with the end sentinel
+    std::vector<int64_t> tile_first;  // ntiles + 1
+    std::vector<int64_t> chunk;       // n_chunks + 1 item indices
+    std::vector<int64_t> chunk_first; // n_seg + 1 chunk indices
+};
+
+// Cut [0, n) at the tile boundaries and at the layer boundaries; index the
+// pieces by tile, and each layer's pieces by level-1 chunk.
+void build_work(const std::vector<int64_t>& off, int32_t n_seg, int64_t head, HostWork* w) {
+    const int64_t n = n_seg ? off[n_seg] : 0;
+    w->items.clear();
+    std::vector<int64_t> first((size_t)n_seg + 1, 0);
     for (int32_t s = 0; s < n_seg; ++s) {
-        (*first)[s] = (int64_t)items->size();
+        first[s] = (int64_t)w->items.size();
         int64_t pos = off[s];
         const int64_t end = off[s + 1];
         while (pos < end) {
-            int64_t tile_end;
-            if (pos < head)
-                tile_end = head;
-            else
-                tile_end = head + ((pos - head) / kLambTile + 1) * kLambTile;
-            items->push_back(zs::LambItem{pos, s, 0});
+            const int64_t tile_end = pos < head ? head : head + ((pos - head) / kLambTile + 1) * kLambTile;
+            w->items.push_back(zs::LambItem{pos, s, 0});
             pos = tile_end < end ? tile_end : end;
         }
     }
-    (*first)[n_seg] = (int64_t)items->size();
-    const int64_t n = n_seg ? off[n_seg] : 0;
-    items->push_back(zs::LambItem{n, -1, 0});
+    first[n_seg] = (int64_t)w->items.size();
+    const int64_t n_items = (int64_t)w->items.size();
+    w->items.push_back(zs::LambItem{n, -1, 0});
+    const int64_t ntiles = tile_count(n, head);
+    w->tile_first.assign((size_t)ntiles + 1, n_items);
+    int64_t next = 0;
+    for (int64_t k = 0; k < n_items; ++k) {
+        const int64_t t = tile_of(w->items[k].start, head);
+        while (next <= t)
+            w->tile_first[next++] = k;
+    }
+    w->chunk.clear();
+    w->chunk_first.assign((size_t)n_seg + 1, 0);
+    for (int32_t s = 0; s < n_seg; ++s) {
+        w->chunk_first[s] = (int64_t)w->chunk.size();
+        for (int64_t k = first[s]; k < first[s + 1]; k += zs::kChunkItems)
+            w->chunk.push_back(k);
+    }
+    w->chunk_first[n_seg] = (int64_t)w->chunk.size();
+    w->chunk.push_back(n_items);
+}
+
+template <typename T>
+int upload(const std::vector<T>& h, T** d) {
+    if (hipMalloc(reinterpret_cast<void**>(d), h.size() * sizeof(T)) != hipSuccess) {
+        *d = nullptr;
+        (void)hipGetLastError();
+        return fail(ZERO_ENOMEM, "zero_lamb: could not allocate a work list of %zu entries", h.size());
+    }
+    HIP_TRY(hipMemcpy(*d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice));
+    return ZERO_OK;
 }
 
 // The work list of `phase` (0..3: vector path with that head; 4: scalar path),
@@ -113,24 +171,20 @@ void build_items(const std::vector<int64_t>& off, int32_t n_seg, int64_t head, s
 int get_work(zero_lamb_plan* plan, int phase, LambWork** out) {
     LambWork& w = plan->work[phase];
     if (!w.built) {
-        std::vector<zs::LambItem> items;
-        std::vector<int64_t> first;
+        HostWork h;
         const int64_t head = phase < 4 ? phase : 0;  // the kernels take the same head
-        build_items(plan->seg_off, plan->n_seg, head, &items, &first);
-        const int64_t n_items = (int64_t)items.size() - 1;
-        if (n_items > plan->max_items)
-            return fail(ZERO_EHIP, "zero_lamb: work list of %lld items exceeds the bound %lld", (long long)n_items,
-                        (long long)plan->max_items);
-        if (hipMalloc(reinterpret_cast<void**>(&w.items), items.size() * sizeof(zs::LambItem)) != hipSuccess ||
-            hipMalloc(reinterpret_cast<void**>(&w.first), first.size() * sizeof(int64_t)) != hipSuccess) {
-            if (w.items) (void)hipFree(w.items);
-            w.items = nullptr;
-            (void)hipGetLastError();
-            return fail(ZERO_ENOMEM, "zero_lamb: could not allocate a work list of %lld items", (long long)n_items);
-        }
-        HIP_TRY(hipMemcpy(w.items, items.data(), items.size() * sizeof(zs::LambItem), hipMemcpyHostToDevice));
-        HIP_TRY(hipMemcpy(w.first, first.data(), first.size() * sizeof(int64_t), hipMemcpyHostToDevice));
+        build_work(plan->seg_off, plan->n_seg, head, &h);
+        const int64_t n_items = (int64_t)h.items.size() - 1, n_chunks = (int64_t)h.chunk.size() - 1;
+        if (n_items > plan->max_items || n_chunks > plan->max_chunks)
+            return fail(ZERO_EHIP, "zero_lamb: work lists (%lld items, %lld chunks) exceed their bounds",
+                        (long long)n_items, (long long)n_chunks);
+        int rc;
+        if ((rc = upload(h.items, &w.items)) || (rc = upload(h.tile_first, &w.tile_first)) ||
+            (rc = upload(h.chunk, &w.chunk)) || (rc = upload(h.chunk_first, &w.chunk_first)))
+            return rc;
         w.n_items = n_items;
+        w.ntiles = (int64_t)h.tile_first.size() - 1;
+        w.n_chunks = n_chunks;
         w.built = true;
     }
     *out = &w;
@@ -224,22 +278,26 @@ unsigned grid_for(int64_t n_items) {
 
 int launch_moments(zero_lamb_plan* plan, const LambWork& w, int phase, const uint16_t* g, const float* th, float* m,
                    float* v, const zs::Result* res, const zs::AdamConst& c, hipStream_t stream) {
-    const unsigned grid = grid_for(w.n_items);
+    const unsigned grid = grid_for(w.ntiles);
     if (phase < 4)
         zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
-            <<<grid, kLambBlock, plan->lds[0], stream>>>(g, th, m, v, w.items, w.n_items, phase, res, c, plan->part);
+            <<<grid, kLambBlock, plan->lds[0], stream>>>(g, th, m, v, w.items, w.tile_first, w.ntiles, plan->n,
+                                                         phase, res, c, plan->part);
     else
         zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
-            <<<grid, kLambBlock, plan->lds_scalar[0], stream>>>(g, th, m, v, w.items, w.n_items, 0, res, c,
-                                                                 plan->part);
+            <<<grid, kLambBlock, plan->lds_scalar[0], stream>>>(g, th, m, v, w.items, w.tile_first, w.ntiles,
+                                                                 plan->n, 0, res, c, plan->part);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
 
 int launch_layer(zero_lamb_plan* plan, const LambWork& w, zs::LayerSums* sums, const zs::Result* res,
                  hipStream_t stream) {
-    const int64_t g = plan->n_seg < 1 ? 1 : (plan->n_seg > kLambMaxBlocks ? kLambMaxBlocks : plan->n_seg);
-    zs::k_lamb_layer<<<(unsigned)g, zs::kLayerBlock, 0, stream>>>(plan->part, w.first, plan->n_seg, sums, res);
+    zs::k_lamb_chunks<<<grid_for(w.n_chunks), zs::kChunkBlock, 0, stream>>>(plan->part, w.chunk, w.n_chunks,
+                                                                            plan->cpart, res);
+    HIP_TRY(hipGetLastError());
+    zs::k_lamb_layer<<<grid_for(plan->n_seg), zs::kLayerBlock, 0, stream>>>(plan->cpart, w.chunk_first,
+                                                                            plan->n_seg, sums, res);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
@@ -247,15 +305,15 @@ int launch_layer(zero_lamb_plan* plan, const LambWork& w, zs::LayerSums* sums, c
 int launch_apply(zero_lamb_plan* plan, const LambWork& w, int phase, float* th, const float* m, const float* v,
                  uint16_t* p, const zs::LayerSums* sums, const zs::Result* res, const zs::AdamConst& c, double lr,
                  double phi_lo, double phi_hi, hipStream_t stream) {
-    const unsigned grid = grid_for(w.n_items);
+    const unsigned grid = grid_for(w.ntiles);
     if (phase < 4)
         zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
-            <<<grid, kLambBlock, plan->lds[1], stream>>>(th, m, v, p, w.items, w.n_items, phase, sums, res, c, lr,
-                                                         phi_lo, phi_hi);
+            <<<grid, kLambBlock, plan->lds[1], stream>>>(th, m, v, p, w.items, w.tile_first, w.ntiles, plan->n,
+                                                         phase, sums, res, c, lr, phi_lo, phi_hi);
     else
         zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
-            <<<grid, kLambBlock, plan->lds_scalar[1], stream>>>(th, m, v, p, w.items, w.n_items, 0, sums, res, c, lr,
-                                                                 phi_lo, phi_hi);
+            <<<grid, kLambBlock, plan->lds_scalar[1], stream>>>(th, m, v, p, w.items, w.tile_first, w.ntiles,
+                                                                 plan->n, 0, sums, res, c, lr, phi_lo, phi_hi);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
@@ -352,11 +410,15 @@ int zero_lamb_plan_create(const int64_t* seg_off, int32_t n_seg, int64_t n, zero
     else
         p->seg_off.assign(1, 0);
     p->max_items = max_items_for(n, n_seg);
+    p->max_chunks = max_chunks_for(p->max_items, n_seg);
     if (n > 0) {
         if (hipMalloc(reinterpret_cast<void**>(&p->part), (size_t)p->max_items * sizeof(zs::LayerSums)) !=
                 hipSuccess ||
+            hipMalloc(reinterpret_cast<void**>(&p->cpart), (size_t)p->max_chunks * sizeof(zs::LayerSums)) !=
+                hipSuccess ||
             hipMalloc(reinterpret_cast<void**>(&p->sums), (size_t)n_seg * sizeof(zs::LayerSums)) != hipSuccess) {
             if (p->part) (void)hipFree(p->part);
+            if (p->cpart) (void)hipFree(p->cpart);
             (void)hipGetLastError();
             return fail(ZERO_ENOMEM, "zero_lamb_plan_create: could not allocate the plan workspace");
         }
@@ -383,11 +445,11 @@ int zero_lamb_plan_destroy(zero_lamb_plan_t* plan) {
             (void)hipSetDevice(plan->dev);
         if (hipDeviceSynchronize() != hipSuccess)
             rc = fail(ZERO_EHIP, "zero_lamb_plan_destroy: device synchronisation failed");
-        for (LambWork& w : plan->work) {
-            if (w.items) (void)hipFree(w.items);
-            if (w.first) (void)hipFree(w.first);
-        }
+        for (LambWork& w : plan->work)
+            for (void* d : {(void*)w.items, (void*)w.tile_first, (void*)w.chunk, (void*)w.chunk_first})
+                if (d) (void)hipFree(d);
         if (plan->part) (void)hipFree(plan->part);
+        if (plan->cpart) (void)hipFree(plan->cpart);
         if (plan->sums) (void)hipFree(plan->sums);
         if (cur != plan->dev)
             (void)hipSetDevice(cur);
