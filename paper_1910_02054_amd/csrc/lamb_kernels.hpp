@@ -123,7 +123,9 @@ __device__ __forceinline__ int64_t tile_range(int64_t b, int64_t head, int64_t n
 }
 
 // ---------------------------------------------------------------------------
-// Moments pass.  Workgroup b (grid-strided over the tiles) owns tile b: thread
+// Moments pass.  Workgroup b (grid-strided over the tiles; with XCD, remapped so
+// that each XCD walks a contiguous run of tiles and the tiles' descriptors,
+// which neighbouring tiles share cache lines of, stay in one L2) owns tile b: thread
 // t covers the U vectors base + 4*(t + u*BLOCK) .. +3.  The data addresses
 // depend on b only, so the loads are issued before the tile's work items
 // (its layer pieces, [tile_first[b], tile_first[b+1]) of the item list) are
@@ -133,7 +135,7 @@ __device__ __forceinline__ int64_t tile_range(int64_t b, int64_t head, int64_t n
 // 8-byte fp16 access; the partial vectors at the array's ends and every
 // element when !VEC (head = 0) take the scalar path.
 // ---------------------------------------------------------------------------
-template <int BLOCK, int U, bool NTL, bool NTS, bool VEC>
+template <int BLOCK, int U, bool NTL, bool NTS, bool VEC, bool XCD>
 __global__ __launch_bounds__(BLOCK) void k_lamb_moments(const uint16_t* __restrict__ g, const float* __restrict__ th,
                                                         float* __restrict__ m, float* __restrict__ v,
                                                         const LambItem* __restrict__ items,
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(BLOCK) void k_lamb_moments(const uint16_t* __restri
     if (res->skip)
         return;
     const float mult = res->mult;
-    for (int64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    for (int64_t b = logical_block<XCD>(); b < ntiles; b += gridDim.x) {
         int64_t ts, te;
         const int64_t base = tile_range<BLOCK, U>(b, head, n, &ts, &te);
         double w2[U][4], u2[U][4];
@@ -267,7 +269,7 @@ __global__ __launch_bounds__(kLayerBlock) void k_lamb_layer(const LayerSums* __r
 // Apply pass: same tile walk as the moments pass; each element moves by its
 // layer piece's step size (theta <- theta - step*u) and gets its fp16 copy.
 // ---------------------------------------------------------------------------
-template <int BLOCK, int U, bool NTL, bool NTS, bool VEC>
+template <int BLOCK, int U, bool NTL, bool NTS, bool VEC, bool XCD>
 __global__ __launch_bounds__(BLOCK) void k_lamb_apply(float* __restrict__ th, const float* __restrict__ m,
                                                       const float* __restrict__ v, uint16_t* __restrict__ p,
                                                       const LambItem* __restrict__ items,
@@ -278,7 +280,7 @@ __global__ __launch_bounds__(BLOCK) void k_lamb_apply(float* __restrict__ th, co
 #pragma clang fp contract(off)
     if (res->skip)
         return;
-    for (int64_t b = blockIdx.x; b < ntiles; b += gridDim.x) {
+    for (int64_t b = logical_block<XCD>(); b < ntiles; b += gridDim.x) {
         int64_t ts, te;
         const int64_t base = tile_range<BLOCK, U>(b, head, n, &ts, &te);
         float t4[U][4], u4[U][4];

@@ -29,7 +29,7 @@
 // ---------------------------------------------------------------------------
 namespace {
 constexpr int kLambBlock = 128, kLambUnroll = 1, kLambPerCU = 16;
-constexpr bool kLambNTL = true, kLambNTS = true;
+constexpr bool kLambNTL = true, kLambNTS = true, kLambXCD = true;
 constexpr int64_t kLambTile = 4 * (int64_t)kLambBlock * kLambUnroll;  // elements per tile
 constexpr int64_t kLambMaxBlocks = 1 << 26;
 constexpr int kPhases = 5;  // vector paths for element misalignment 0..3, then the scalar path
@@ -81,11 +81,11 @@ zero_lamb_profile_t g_lprof_acc = {0, 0.0, 0.0, 0.0, 0.0};
 
 template <bool VEC>
 const void* moments_kernel() {
-    return reinterpret_cast<const void*>(zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC>);
+    return reinterpret_cast<const void*>(zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC, kLambXCD>);
 }
 template <bool VEC>
 const void* apply_kernel() {
-    return reinterpret_cast<const void*>(zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC>);
+    return reinterpret_cast<const void*>(zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC, kLambXCD>);
 }
 
 // Upper bound on the items of any alignment: one per tile the shard touches
@@ -276,15 +276,23 @@ unsigned grid_for(int64_t n_items) {
     return (unsigned)(b > kLambMaxBlocks ? kLambMaxBlocks : b);
 }
 
+// Grid of the tile passes: a multiple of 8 (the XCD count) so that the XCD
+// remapping of workgroups is a bijection; the extra workgroups find no tile.
+unsigned tile_grid(int64_t ntiles) {
+    int64_t b = ntiles < 1 ? 1 : ntiles;
+    b = b > kLambMaxBlocks ? kLambMaxBlocks : b;
+    return (unsigned)((b + 7) / 8 * 8);
+}
+
 int launch_moments(zero_lamb_plan* plan, const LambWork& w, int phase, const uint16_t* g, const float* th, float* m,
                    float* v, const zs::Result* res, const zs::AdamConst& c, hipStream_t stream) {
-    const unsigned grid = grid_for(w.ntiles);
+    const unsigned grid = tile_grid(w.ntiles);
     if (phase < 4)
-        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
+        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true, kLambXCD>
             <<<grid, kLambBlock, plan->lds[0], stream>>>(g, th, m, v, w.items, w.tile_first, w.ntiles, plan->n,
                                                          phase, res, c, plan->part);
     else
-        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
+        zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false, kLambXCD>
             <<<grid, kLambBlock, plan->lds_scalar[0], stream>>>(g, th, m, v, w.items, w.tile_first, w.ntiles,
                                                                  plan->n, 0, res, c, plan->part);
     HIP_TRY(hipGetLastError());
@@ -305,13 +313,13 @@ int launch_layer(zero_lamb_plan* plan, const LambWork& w, zs::LayerSums* sums, c
 int launch_apply(zero_lamb_plan* plan, const LambWork& w, int phase, float* th, const float* m, const float* v,
                  uint16_t* p, const zs::LayerSums* sums, const zs::Result* res, const zs::AdamConst& c, double lr,
                  double phi_lo, double phi_hi, hipStream_t stream) {
-    const unsigned grid = grid_for(w.ntiles);
+    const unsigned grid = tile_grid(w.ntiles);
     if (phase < 4)
-        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true>
+        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, true, kLambXCD>
             <<<grid, kLambBlock, plan->lds[1], stream>>>(th, m, v, p, w.items, w.tile_first, w.ntiles, plan->n,
                                                          phase, sums, res, c, lr, phi_lo, phi_hi);
     else
-        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false>
+        zs::k_lamb_apply<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, false, kLambXCD>
             <<<grid, kLambBlock, plan->lds_scalar[1], stream>>>(th, m, v, p, w.items, w.tile_first, w.ntiles,
                                                                  plan->n, 0, sums, res, c, lr, phi_lo, phi_hi);
     HIP_TRY(hipGetLastError());
