@@ -25,6 +25,8 @@
  *     device is the current HIP device of the calling thread; a stream of
  *     another device is rejected with ZERO_EINVAL.
  *   - Concurrent calls are serialised per (device, stream) by the library.
+ *     The workspace is keyed by the stream handle: do not destroy a stream
+ *     while calls on it are in flight (a new stream may reuse its handle).
  */
 #ifndef ZERO_SHARD_H
 #define ZERO_SHARD_H
@@ -232,7 +234,9 @@ int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, doubl
  * 256 elements plus 32 bytes per layer, and the work lists, built per array
  * alignment on first use); zero_lamb_plan_destroy waits for the device and
  * frees it.  Calls on one plan are serialised by the library; a call on a
- * different stream from the plan's previous call first waits for that stream.
+ * different stream from the plan's previous call first waits for the device
+ * to finish its queued work (hipDeviceSynchronize), so keep a plan on one
+ * stream in a loop.
  * Returns ZERO_OK, ZERO_EINVAL (bad table, n outside [0, 2^40], NULL out) or
  * ZERO_ENOMEM / ZERO_EHIP. */
 typedef struct zero_lamb_plan zero_lamb_plan_t;

@@ -262,10 +262,12 @@ int check_layer_sums(const char* fn, const zero_lamb_plan_t* plan, const void* l
 }
 
 // Work queued on the plan's previous stream must finish before another
-// stream reuses the plan's partials and sums.
+// stream reuses the plan's partials and sums.  A device-wide wait (rare: only
+// when the stream changes) also covers a previous stream the caller has since
+// destroyed.
 int switch_stream(zero_lamb_plan* plan, hipStream_t stream) {
     if (plan->used && plan->last_stream != stream)
-        HIP_TRY(hipStreamSynchronize(plan->last_stream));
+        HIP_TRY(hipDeviceSynchronize());
     plan->used = true;
     plan->last_stream = stream;
     return ZERO_OK;
