@@ -1,5 +1,6 @@
 """bench.py's contract pieces that need no GPU: it refuses more than one GPU with a
-message, and it reads the committed counter summary only for the current kernels."""
+message, and it reads the committed counter summaries (Adam update, LAMB moments pass) only
+for the kernels and launch policy they were taken on."""
 import os
 import subprocess
 import sys
@@ -31,3 +32,26 @@ def test_traffic_summary_matches_the_kernel_sources_or_is_ignored(tmp_path, monk
                     % bench.kernel_source_hash())
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(good))
     assert bench.measured_traffic(250_000_000) == 7e9
+
+
+def test_lamb_traffic_summary_matches_the_kernel_sources_or_is_ignored(tmp_path, monkeypatch):
+    t = bench.measured_lamb_traffic(250_000_000)
+    if t is not None:  # present and current: within 1 % of the moments pass's 22 B/element
+        assert abs(t / (22 * 250_000_000) - 1) < 0.01
+    assert bench.measured_lamb_traffic(12345) is None
+    stale = tmp_path / "t.txt"
+    stale.write_text("kernel_source_sha256_16: %s\nshard_numel: 250000000\nmoments_bytes_per_launch: 5.5e9\n"
+                     % bench.kernel_source_hash())  # the Adam hash is not the LAMB kernels' hash
+    monkeypatch.setattr(bench, "LAMB_TRAFFIC_FILE", str(stale))
+    assert bench.measured_lamb_traffic(250_000_000) is None
+    good = tmp_path / "g.txt"
+    good.write_text("kernel_source_sha256_16: %s\nshard_numel: 250000000\nmoments_bytes_per_launch: 5.5e9\n"
+                    % bench.lamb_kernel_source_hash())
+    monkeypatch.setattr(bench, "LAMB_TRAFFIC_FILE", str(good))
+    assert bench.measured_lamb_traffic(250_000_000) == 5.5e9
+
+
+def test_kernel_hashes_ignore_comments_but_not_code():
+    src = "int a = 1; // one\n/* block */ int b = 2;\n\n"
+    assert bench._code_only(src) == bench._code_only("int a = 1;\nint b = 2;")
+    assert bench._code_only(src) != bench._code_only("int a = 1;\nint b = 3;")
