@@ -1,0 +1,87 @@
+"""The Python binding on the CPU: argument marshalling fails loudly (no host
+fallback exists), and the LAMB plan wrapper validates layer tables before
+anything reaches a device."""
+import types
+
+import numpy as np
+import pytest
+import torch
+
+
+@pytest.fixture(scope="module")
+def zb():
+    from paper_1910_02054_amd import build as b
+    if b.is_stale():
+        b.build()
+    from paper_1910_02054_amd import binding
+    return binding
+
+
+def _cpu_shard(n):
+    return (torch.zeros(n, dtype=torch.float16), torch.zeros(n), torch.zeros(n), torch.zeros(n),
+            torch.zeros(n, dtype=torch.float16))
+
+
+def test_host_tensors_are_refused(zb):
+    with pytest.raises(TypeError, match="device tensor"):
+        zb.zero_shard_step(*_cpu_shard(8), 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
+    with pytest.raises(TypeError, match="device tensor"):
+        zb.zero_shard_stats(torch.zeros(8, dtype=torch.float16))
+    with pytest.raises(TypeError, match="device tensor"):
+        zb.zero_shard_apply(*_cpu_shard(8), 1.0, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
+
+
+def test_wrong_dtypes_are_refused(zb):
+    g, th, m, v, p = _cpu_shard(8)
+    # each argument's dtype is checked before its device, in argument order
+    with pytest.raises(TypeError, match="grad16: dtype"):
+        zb.zero_shard_step(th, th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
+    with pytest.raises(TypeError, match="grad16: dtype"):
+        zb.zero_shard_stats(th)
+
+
+def test_shard_tensors_of_different_lengths_are_refused(zb):
+    g, th, m, v, p = _cpu_shard(8)
+    with pytest.raises(ValueError, match="differ in length"):
+        zb.zero_shard_step(g, th, m[:4], v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
+
+
+@pytest.mark.parametrize("offs", [[0, 5, 5, 10], [1, 10], [0, 7, 3, 10]])
+def test_lamb_plan_rejects_bad_tables(zb, offs):
+    with pytest.raises(zb.ZeroError) as e:
+        zb.LambPlan(offs)
+    assert e.value.code == zb.ZERO_EINVAL
+
+
+def test_lamb_plan_rejects_malformed_input(zb):
+    with pytest.raises(ValueError):
+        zb.LambPlan([])
+    with pytest.raises(ValueError):
+        zb.LambPlan(np.zeros((2, 2), np.int64))
+
+
+def test_lamb_plan_needs_a_device_for_a_valid_table(zb):
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(zb.ZeroError) as e:
+        zb.LambPlan([0, 10])
+    assert e.value.code == zb.ZERO_EHIP
+
+
+def test_lamb_wrappers_check_lengths_against_the_plan(zb):
+    plan = types.SimpleNamespace(n=16, n_seg=2, handle=None)  # stands in for a plan; no call reaches C
+    g, th, m, v, p = _cpu_shard(8)
+    with pytest.raises(ValueError, match="plan's n"):
+        zb.zero_lamb_step(plan, g, th, m, v, p, 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 1.0, 1.0)
+    g, th, m, v, p = _cpu_shard(16)
+    with pytest.raises(ValueError, match="2 \\* n_seg"):
+        zb.zero_lamb_moments(plan, g, th, m, v, 1.0, 0.9, 0.999, 1e-6, 0.0, 1, 1.0, 1.0,
+                             torch.zeros(3, dtype=torch.float64))
+    with pytest.raises(TypeError, match="device tensor"):
+        zb.zero_lamb_step(plan, g, th, m, v, p, 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 1.0, 1.0)
+
+
+def test_exports_match_the_loaded_library(zb):
+    lib = zb.raw_library()
+    for name in zb.EXPORTS:
+        assert hasattr(lib, name), name
