@@ -59,16 +59,18 @@ def test_encode_special_values():
 
 
 def test_encode_exhaustive_over_all_fp32_patterns():
-    # Every one of the 2^32 fp32 bit patterns, in parallel chunks; NaNs must stay NaN.
+    # Every one of the 2^32 fp32 bit patterns, in parallel chunks, against torch's CPU
+    # float->half conversion (round to nearest even; numpy's cast agrees with it and is
+    # checked on a sample in test_encode_matches_numpy_on_a_sample); NaNs must stay NaN.
     from concurrent.futures import ThreadPoolExecutor
+    import torch
     chunk = 1 << 26
 
     def check(c):
-        bits = np.arange(c * chunk, (c + 1) * chunk, dtype=np.uint64).astype(np.uint32)
+        bits = np.arange(chunk, dtype=np.uint32) + np.uint32(c * chunk)
         x = bits.view(np.float32)
         got = oracle.f32_to_f16_array(x)
-        with np.errstate(over="ignore"):
-            ref = x.astype(np.float16).view(np.uint16)
+        ref = torch.from_numpy(x).to(torch.float16).view(torch.int16).numpy().view(np.uint16)
         nan = np.isnan(x)
         bad = np.flatnonzero((got != ref) & ~nan)
         nan_ok = bool(np.all((got[nan] & 0x7C00) == 0x7C00) and np.all((got[nan] & 0x3FF) != 0))
@@ -79,3 +81,15 @@ def test_encode_exhaustive_over_all_fp32_patterns():
         results = list(ex.map(check, range((1 << 32) // chunk)))
     assert sum(r[0] for r in results) == 0, [hex(r[1]) for r in results if r[1] is not None][:5]
     assert all(r[2] for r in results)
+
+
+def test_encode_matches_numpy_on_a_sample():
+    # numpy's own float16 cast as a second, independent reference on random patterns
+    r = np.random.default_rng(21)
+    bits = r.integers(0, 1 << 32, size=1 << 21, dtype=np.uint64).astype(np.uint32)
+    x = bits.view(np.float32)
+    got = oracle.f32_to_f16_array(x)
+    with np.errstate(over="ignore"):
+        ref = x.astype(np.float16).view(np.uint16)
+    keep = ~np.isnan(x)
+    assert np.array_equal(got[keep], ref[keep])
