@@ -170,6 +170,9 @@ def main():
                     help="also run the library's copy kernel over this many MiB (counter calibration)")
     ap.add_argument("--optimizer", choices=("adam", "lamb"), default="adam",
                     help="adam: the mixed-precision Adam shard step; lamb: LAMB over the shard's layer table")
+    ap.add_argument("--split-phase", action="store_true",
+                    help="adam only: each step as zero_shard_stats -> (one rank: the local sum is the global one) "
+                         "-> zero_shard_apply, the seam a multi-rank run exchanges 8 bytes at")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -211,9 +214,17 @@ def main():
         seg = workloads.layer_offsets_in(sizes, lay.offset, lay.offset + n)
         plan = zb.LambPlan(seg)
 
+    if args.split_phase and lamb:
+        print("bench.py: --split-phase is measured for the Adam step only", file=sys.stderr)
+        sys.exit(2)
+
     def step():
         d_g = d_gs[scaler.t_next % 2]
-        if lamb:
+        if args.split_phase:
+            local = zb.zero_shard_stats(d_g, stream=stream)
+            flag = zb.zero_shard_apply(d_g, d_theta, d_m, d_v, d_p, local, w.lr, w.beta1, w.beta2, w.eps,
+                                       w.weight_decay, scaler.t_next, scaler.scale, w.clip, stream=stream)
+        elif lamb:
             flag = zb.zero_lamb_step(plan, d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps,
                                      w.weight_decay, scaler.t_next, scaler.scale, w.clip, stream=stream)
         else:
@@ -304,6 +315,9 @@ def main():
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
     }
+    if args.split_phase:
+        out["config"].update(path="split phase: zero_shard_stats, host-side global sum, zero_shard_apply")
+        out["kernel_ms"]["stats_and_finalize"] = None  # timed per apply: only the result-record kernel
     if lamb:
         out["config"].update(optimizer="lamb", layers=int(seg.size - 1))
         out["lamb_apply"] = {"kernel": "k_lamb_apply", "achieved_gbps": apply_gbps,

@@ -300,7 +300,9 @@ const char* zero_last_error(void);
 /* Kernel timing with HIP events on the call's own stream.  With every = k > 0,
  * one zero_shard_step in k on each stream records events before its
  * statistics kernels, before its update kernel and after it (each event marker
- * costs the GPU a few microseconds, hence the sampling); every = 0 disables.
+ * costs the GPU a few microseconds, hence the sampling); zero_shard_apply
+ * calls are sampled the same way, their statistics interval covering only the
+ * result-record kernel; every = 0 disables.
  * zero_profile_read waits for the recorded work, then returns the summed
  * durations and the number of profiled steps since enabling (or the last read)
  * and resets them.  ZERO_EINVAL for every < 0. */

@@ -444,7 +444,9 @@ int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out) {
 
 // Profiling events of one step (taken from a pool while profiling is on).
 // Returns false when profiling is off; rec->end == nullptr signals failure.
-bool prof_begin(Ctx* ctx, ProfRec* rec) {
+// With chain, a step that directly follows a profiled step on the stream takes
+// that step's end event as its start.
+bool prof_begin(Ctx* ctx, ProfRec* rec, bool chain = true) {
     std::lock_guard<std::mutex> plk(g_prof_mu);
     if (g_prof_every <= 0)
         return false;
@@ -452,7 +454,7 @@ bool prof_begin(Ctx* ctx, ProfRec* rec) {
         ctx->prof_last_end = nullptr;  // the chain of back-to-back profiled steps is broken
         return false;
     }
-    rec->own_start = ctx->prof_last_end == nullptr;
+    rec->own_start = !chain || ctx->prof_last_end == nullptr;
     rec->start = rec->own_start ? prof_event() : ctx->prof_last_end;
     rec->mid = prof_event();
     rec->end = prof_event();
@@ -672,9 +674,26 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
     const uint32_t seq = next_seq(ctx);
+    // sampled timing as in zero_shard_step, unchained: the "statistics" interval
+    // here is the result-record kernel only (the statistics ran in zero_shard_stats)
+    ProfRec pr{};
+    const bool prof = prof_begin(ctx, &pr, false);
+    if (prof && !pr.end)
+        return fail(ZERO_EHIP, "zero_shard_apply: could not create a profiling event");
+    if (prof && pr.own_start)
+        HIP_TRY(hipEventRecord(pr.start, stream));
     zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
     HIP_TRY(hipGetLastError());
-    return launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.mid, stream));
+    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
+        return rc;
+    if (prof) {
+        HIP_TRY(hipEventRecord(pr.end, stream));
+        if ((rc = prof_end(ctx, pr)))
+            return rc;
+    }
+    return ZERO_OK;
 }
 
 int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,

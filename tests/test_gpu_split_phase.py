@@ -166,3 +166,28 @@ def test_multi_step_ranks_follow_the_oracle(env):
         assert skip == 0
         d = H.compare_state([b.download()[:psi] for b in bufs[1:]], ref)
         say("step", t, d)
+
+
+def test_apply_is_profiled_unchained(env):
+    # sampled timing of zero_shard_apply: the interval before the update covers only the
+    # result-record kernel, not the statistics that ran in zero_shard_stats
+    torch, zb, dev = env
+    n = 4_000_000
+    g16, theta, m, v = workloads.random_case(202, n)
+    bufs = [H.Guarded(torch, n, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                                  torch.float16)]
+    for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    zb.zero_profile_read()
+    zb.zero_profile_enable(1)
+    try:
+        for t in range(1, 4):
+            local = zb.zero_shard_stats(bufs[0].view)
+            assert zb.zero_shard_apply(*(b.view for b in bufs), local, **{k: HP[k] for k in ("lr", "beta1", "beta2",
+                                                                                             "eps", "weight_decay")},
+                                       step=t, loss_scale=2.0 ** 16, clip=1.0) == 0
+        p = zb.zero_profile_read()
+    finally:
+        zb.zero_profile_enable(0)
+    say("apply profile", p.steps, p.stats_ms, p.update_ms)
+    assert p.steps == 3 and p.update_ms > 0 and p.stats_ms < p.update_ms
