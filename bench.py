@@ -173,6 +173,9 @@ def main():
     ap.add_argument("--split-phase", action="store_true",
                     help="adam only: each step as zero_shard_stats -> (one rank: the local sum is the global one) "
                          "-> zero_shard_apply, the seam a multi-rank run exchanges 8 bytes at")
+    ap.add_argument("--async-seam", action="store_true",
+                    help="with --split-phase: the asynchronous calls (sums in device memory, no host wait; the "
+                         "skip flags are checked after the timed region)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -217,9 +220,25 @@ def main():
     if args.split_phase and lamb:
         print("bench.py: --split-phase is measured for the Adam step only", file=sys.stderr)
         sys.exit(2)
+    if args.async_seam and not args.split_phase:
+        print("bench.py: --async-seam needs --split-phase", file=sys.stderr)
+        sys.exit(2)
+    d_sum = torch.zeros(1, dtype=torch.float64, device=dev)
+    d_flags = torch.full((args.warmup + args.steps,), -1, dtype=torch.int32, device=dev)
+    calls = [0]
 
     def step():
         d_g = d_gs[scaler.t_next % 2]
+        if args.async_seam:
+            # one rank: the local sum in device memory is the global one; no host wait, so the
+            # flag is read after the timed region and t advances as if every step applied
+            zb.zero_shard_stats_async(d_g, d_sum, stream=stream)
+            zb.zero_shard_apply_async(d_g, d_theta, d_m, d_v, d_p, d_sum, w.lr, w.beta1, w.beta2, w.eps,
+                                      w.weight_decay, scaler.t_next, scaler.scale, w.clip,
+                                      skipped=d_flags[calls[0]:calls[0] + 1], stream=stream)
+            calls[0] += 1
+            scaler.update(False)
+            return 0
         if args.split_phase:
             local = zb.zero_shard_stats(d_g, stream=stream)
             flag = zb.zero_shard_apply(d_g, d_theta, d_m, d_v, d_p, local, w.lr, w.beta1, w.beta2, w.eps,
@@ -272,6 +291,8 @@ def main():
     zb.zero_profile_enable(False)
     prof = zb.zero_profile_read()
     lprof = zb.zero_lamb_profile_read()
+    if args.async_seam:
+        skips = int((d_flags != 0).sum().item())
     if skips:
         print("bench.py: %d timed steps skipped on overflow; the measurement is invalid" % skips, file=sys.stderr)
         sys.exit(1)
@@ -316,7 +337,9 @@ def main():
                      "traffic": traffic},
     }
     if args.split_phase:
-        out["config"].update(path="split phase: zero_shard_stats, host-side global sum, zero_shard_apply")
+        out["config"].update(path="split phase: zero_shard_stats_async, device-resident global sum, "
+                                  "zero_shard_apply_async (no host wait)" if args.async_seam else
+                                  "split phase: zero_shard_stats, host-side global sum, zero_shard_apply")
         out["kernel_ms"]["stats_and_finalize"] = None  # timed per apply: only the result-record kernel
     if lamb:
         out["config"].update(optimizer="lamb", layers=int(seg.size - 1))

@@ -142,6 +142,29 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
                      int64_t n, double global_sumsq, double lr, double beta1, double beta2, double eps,
                      double weight_decay, int64_t step, double loss_scale, double clip, void* stream);
 
+/* Asynchronous split phase: the same kernels as zero_shard_stats /
+ * zero_shard_apply, with the scalars in DEVICE memory and no host wait, so both
+ * calls only enqueue work on `stream` and return.  A device-side exchange of
+ * the per-rank sums (an all-reduce or all-gather on the same stream, summed in
+ * rank order so that every rank holds the same bits) can sit between them, and
+ * the step never makes the host wait for the GPU.
+ *   zero_shard_stats_async writes this shard's sum of grad16^2 (fp64; +inf or
+ *   NaN on overflow, as zero_shard_stats returns it) to *local_sumsq (device,
+ *   8-byte aligned); n = 0 writes 0.
+ *   zero_shard_apply_async reads the global sum from *global_sumsq (device) when
+ *   its kernels run; a non-finite, negative or NaN value skips the update (no
+ *   state byte written) exactly as an overflow does.  The skip decision (1 or
+ *   0) is stored to *skipped when skipped is not NULL (device memory, or
+ *   mapped host memory from hipHostMalloc that the host reads after the stream
+ *   has reached this call).  The loss scaler is the caller's, with that flag.
+ * Argument checks, the allocation checks included, are those of the
+ * synchronous calls; returns ZERO_OK (enqueued) or an error. */
+int zero_shard_stats_async(const uint16_t* grad16, int64_t n, double* local_sumsq, void* stream);
+int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                           int64_t n, const double* global_sumsq, double lr, double beta1, double beta2, double eps,
+                           double weight_decay, int64_t step, double loss_scale, double clip, int32_t* skipped,
+                           void* stream);
+
 /* The array checks of zero_shard_step without launching anything: n range,
  * NULL pointers, alignment, that each array [p, p + n*size) lies inside one
  * GPU-accessible allocation (hipMemGetAddressRange), then overlap.
@@ -300,9 +323,9 @@ const char* zero_last_error(void);
 /* Kernel timing with HIP events on the call's own stream.  With every = k > 0,
  * one zero_shard_step in k on each stream records events before its
  * statistics kernels, before its update kernel and after it (each event marker
- * costs the GPU a few microseconds, hence the sampling); zero_shard_apply
- * calls are sampled the same way, their statistics interval covering only the
- * result-record kernel; every = 0 disables.
+ * costs the GPU a few microseconds, hence the sampling); zero_shard_apply and
+ * zero_shard_apply_async calls are sampled the same way, their statistics
+ * interval covering only the result-record kernel; every = 0 disables.
  * zero_profile_read waits for the recorded work, then returns the summed
  * durations and the number of profiled steps since enabling (or the last read)
  * and resets them.  ZERO_EINVAL for every < 0. */

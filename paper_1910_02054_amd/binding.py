@@ -65,6 +65,9 @@ _lib.zero_last_error.restype = ctypes.c_char_p
 _lib.zero_profile_enable.argtypes = [_i32]
 _lib.zero_profile_read.argtypes = [ctypes.POINTER(Profile)]
 _lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
+_lib.zero_shard_stats_async.argtypes = [_P, _i64, _P, _P]
+_lib.zero_shard_apply_async.argtypes = [_P, _P, _P, _P, _P, _i64, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl,
+                                        _P, _P]
 _lib.zero_lamb_plan_create.argtypes = [_P, _i32, _i64, ctypes.POINTER(_P)]
 _lib.zero_lamb_plan_destroy.argtypes = [_P]
 _lib.zero_lamb_step.argtypes = [_P, _P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _dbl, _dbl, _P]
@@ -75,14 +78,16 @@ for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
            "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step",
-           "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read"):
+           "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async",
+           "zero_shard_apply_async"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
            "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
            "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
            "zero_profile_read", "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy",
-           "zero_lamb_step", "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read")
+           "zero_lamb_step", "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read",
+           "zero_shard_stats_async", "zero_shard_apply_async")
 
 
 def _check(rc):
@@ -169,6 +174,37 @@ def zero_shard_apply(grad16, master32, m32, v32, param16_out, global_sumsq, lr, 
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(global_sumsq), float(lr),
         float(beta1), float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
         _stream(stream)))
+
+
+def zero_shard_stats_async(grad16, local_sumsq, n=None, stream=None):
+    """Enqueue the shard's sum of squares into local_sumsq (a float64 device tensor
+    of one element, or a device address); returns without waiting."""
+    import torch
+    if n is None:
+        n = grad16.numel()
+    _check(_lib.zero_shard_stats_async(_addr(grad16, (torch.float16, torch.int16), "grad16"), int(n),
+                                       _addr(local_sumsq, (torch.float64,), "local_sumsq"), _stream(stream)))
+
+
+def zero_shard_apply_async(grad16, master32, m32, v32, param16_out, global_sumsq, lr, beta1, beta2, eps,
+                           weight_decay, step, loss_scale, clip, skipped=None, n=None, stream=None):
+    """Enqueue the update with the global sum read from device memory (global_sumsq:
+    a float64 device tensor or address); the skip flag goes to `skipped` (an int32
+    device tensor, a mapped host address, or None).  Returns without waiting."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    if n is None:
+        n = grad16.numel()
+        for t in (master32, m32, v32, param16_out):
+            if t.numel() != n:
+                raise ValueError("shard tensors differ in length")
+    _check(_lib.zero_shard_apply_async(
+        _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n),
+        _addr(global_sumsq, (torch.float64,), "global_sumsq"), float(lr), float(beta1), float(beta2), float(eps),
+        float(weight_decay), int(step), float(loss_scale), float(clip),
+        _addr(skipped, (torch.int32,), "skipped"), _stream(stream)))
 
 
 def zero_shard_validate(grad16, master32, m32, v32, param16_out, n):

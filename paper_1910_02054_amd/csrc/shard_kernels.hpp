@@ -242,6 +242,48 @@ constexpr int kFinalBlock = 256;
     }
 }
 
+// One double into device memory (the empty shard's local sum, enqueued in order).
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_value(double* __restrict__ out, double value) {
+    if (threadIdx.x == 0)
+        *out = value;
+}
+
+// Statistics total into caller device memory (the asynchronous split phase:
+// no result record, no host copy).
+[[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize_sum(
+    const Partial* __restrict__ part, int nparts, double* __restrict__ out) {
+    double s0 = 0.0, s1 = 0.0;
+    int i = threadIdx.x;
+    for (; i + kFinalBlock < nparts; i += 2 * kFinalBlock) {
+        s0 += part[i].sumsq;
+        s1 += part[i + kFinalBlock].sumsq;
+    }
+    if (i < nparts)
+        s0 += part[i].sumsq;
+    const double tot = block_sum<kFinalBlock>(s0 + s1);
+    if (threadIdx.x == 0)
+        *out = tot;
+}
+
+// Result record from a global sum of squares in device memory (the
+// asynchronous split phase); the skip flag also goes to `skipped` when given
+// (device or host-mapped memory).
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_result_dev(Result* __restrict__ res,
+                                                                                const double* __restrict__ global,
+                                                                                double loss_scale, double clip,
+                                                                                int32_t* __restrict__ skipped,
+                                                                                uint32_t seq) {
+    if (threadIdx.x == 0) {
+        double g = *global;
+        if (!(g >= 0.0))
+            g = __builtin_inf();  // negative or NaN: not a sum of squares, skip like an overflow
+        const Result r = make_result(g, loss_scale, clip, seq);
+        *res = r;
+        if (skipped)
+            *skipped = r.skip;
+    }
+}
+
 // Result record from a global sum of squares supplied by the caller (the
 // split-phase step: each rank's local sums combined outside the library).
 [[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_result(Result* __restrict__ res,

@@ -696,6 +696,109 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     return ZERO_OK;
 }
 
+int zero_shard_stats_async(const uint16_t* grad16, int64_t n, double* local_sumsq, void* stream_) {
+    const char* fn = "zero_shard_stats_async";
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "%s: n=%lld outside [0, 2^40]", fn, (long long)n);
+    if (n > 0 && (!grad16 || reinterpret_cast<uintptr_t>(grad16) % 2))
+        return fail(ZERO_EINVAL, "%s: grad16 is NULL or not 2-byte aligned", fn);
+    if (!local_sumsq || reinterpret_cast<uintptr_t>(local_sumsq) % 8)
+        return fail(ZERO_EINVAL, "%s: local_sumsq must be an 8-byte aligned device pointer", fn);
+    if (n > 0 && overlaps(reinterpret_cast<uintptr_t>(grad16), 2 * (size_t)n,
+                          reinterpret_cast<uintptr_t>(local_sumsq), sizeof(double)))
+        return fail(ZERO_EINVAL, "%s: local_sumsq overlaps grad16", fn);
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    int rc = get_ctx(stream, &ctx);
+    if (rc)
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    {
+        const void* ptrs[2] = {local_sumsq, grad16};
+        const size_t bytes[2] = {sizeof(double), 2 * (size_t)n};
+        if ((rc = check_ranges(fn, ptrs, bytes, n > 0 ? 2 : 1)))
+            return rc;
+    }
+    if (n == 0) {
+        zs::k_set_value<<<1, 64, 0, stream>>>(local_sumsq, 0.0);
+        HIP_TRY(hipGetLastError());
+        return ZERO_OK;
+    }
+    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
+    zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
+        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+    HIP_TRY(hipGetLastError());
+    zs::k_finalize_sum<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, local_sumsq);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                           int64_t n, const double* global_sumsq, double lr, double beta1, double beta2, double eps,
+                           double weight_decay, int64_t step, double loss_scale, double clip, int32_t* skipped,
+                           void* stream_) {
+    const char* fn = "zero_shard_apply_async";
+    int rc = check_update_args(fn, grad16, master32, m32, v32, param16_out, n, lr, beta1, beta2, eps, weight_decay,
+                               step, loss_scale, clip);
+    if (rc)
+        return rc;
+    if (!global_sumsq || reinterpret_cast<uintptr_t>(global_sumsq) % 8)
+        return fail(ZERO_EINVAL, "%s: global_sumsq must be an 8-byte aligned device pointer", fn);
+    if (skipped && reinterpret_cast<uintptr_t>(skipped) % 4)
+        return fail(ZERO_EINVAL, "%s: skipped must be 4-byte aligned", fn);
+    {
+        // the scalars must not alias the state the update writes
+        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
+                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
+                                reinterpret_cast<uintptr_t>(param16_out)};
+        const size_t esz[5] = {2, 4, 4, 4, 2};
+        for (int i = 0; i < 5 && n > 0; ++i) {
+            if (overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(global_sumsq), sizeof(double)) ||
+                (skipped && overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(skipped), 4)))
+                return fail(ZERO_EINVAL, "%s: global_sumsq or skipped overlaps array %d", fn, i);
+        }
+    }
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    {
+        const void* ptrs[2] = {global_sumsq, skipped};
+        const size_t bytes[2] = {sizeof(double), sizeof(int32_t)};
+        if ((rc = check_ranges(fn, ptrs, bytes, skipped ? 2 : 1)))
+            return rc;
+    }
+    if (n > 0 && (rc = check_shard_ranges_cached(ctx, fn, grad16, master32, m32, v32, param16_out, n)))
+        return rc;
+    const uint32_t seq = next_seq(ctx);
+    if (n == 0) {
+        zs::k_set_result_dev<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, skipped, seq);
+        HIP_TRY(hipGetLastError());
+        return ZERO_OK;
+    }
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    ProfRec pr{};
+    const bool prof = prof_begin(ctx, &pr, false);  // unchained, as zero_shard_apply
+    if (prof && !pr.end)
+        return fail(ZERO_EHIP, "%s: could not create a profiling event", fn);
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.start, stream));
+    zs::k_set_result_dev<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, skipped, seq);
+    HIP_TRY(hipGetLastError());
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.mid, stream));
+    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
+        return rc;
+    if (prof) {
+        HIP_TRY(hipEventRecord(pr.end, stream));
+        if ((rc = prof_end(ctx, pr)))
+            return rc;
+    }
+    return ZERO_OK;
+}
+
 int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
                         const uint16_t* param16_out, int64_t n) {
     // The allocation check comes before the disjointness check here, so an n that

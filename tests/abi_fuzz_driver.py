@@ -80,4 +80,11 @@ for _ in range(500):
     L.zero_lamb_moments(None, *G[:4], 1.0, 0.9, 0.999, 1e-6, 0.0, 1, 65536.0, 1.0, G[4], None)
     L.zero_lamb_apply(None, *G[1:], 1.0, G[0], 1e-3, 0.9, 0.999, 1e-6, 0.0, 1, 0.0, float("inf"), None)
     L.zero_last_error()
+L.zero_shard_stats_async.argtypes = [P, i64, P, P]
+L.zero_shard_apply_async.argtypes = [P, P, P, P, P, i64, P, dbl, dbl, dbl, dbl, dbl, i64, dbl, dbl, P, P]
+for _ in range(2000):
+    L.zero_shard_stats_async(G[0] + r.choice([0, 1]), r.choice([-1, 10, 1 << 41]), r.choice([None, G[1] + 4, G[0]]), None)
+    L.zero_shard_apply_async(*G, r.choice([-1, 10]), r.choice([None, 0x60000004]), 1e-3, 0.9, 0.999, 1e-8, 0.0,
+                             r.choice([0, -1]), 65536.0, 1.0, r.choice([None, 0x70000002]), None)
+    L.zero_last_error()
 print("driver done", bad, "rejected or empty calls")

@@ -223,3 +223,20 @@ def test_lamb_calls_reject_a_null_plan(zb):
     assert "NULL plan" in zb.zero_last_error()
     p = zb.LambProfile()
     assert lib.zero_lamb_profile_read(ctypes.byref(p)) == zb.ZERO_OK and p.steps == 0
+
+
+def test_async_split_rejects_without_a_gpu(zb):
+    lib = zb.raw_library()
+    G = [0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000]
+    assert lib.zero_shard_stats_async(G[0], 10, None, None) == zb.ZERO_EINVAL          # NULL sum
+    assert lib.zero_shard_stats_async(G[0], 10, G[1] + 4, None) == zb.ZERO_EINVAL      # misaligned sum
+    assert lib.zero_shard_stats_async(G[0] + 1, 10, G[1], None) == zb.ZERO_EINVAL      # misaligned grad
+    assert lib.zero_shard_stats_async(G[0], -1, G[1], None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_stats_async(G[0], 10, G[0] + 8, None) == zb.ZERO_EINVAL      # sum inside grad16
+    hp = (1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 65536.0, 1.0)
+    assert lib.zero_shard_apply_async(*G, 10, None, *hp, None, None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_apply_async(*G, 10, 0x60000000 + 4, *hp, None, None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_apply_async(*G, 10, 0x60000000, *hp, 0x70000000 + 2, None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_apply_async(*G, 10, G[1] + 8, *hp, None, None) == zb.ZERO_EINVAL  # sum inside master
+    assert lib.zero_shard_apply_async(*G, 10, 0x60000000, 1e-3, 0.9, 0.999, 1e-8, 0.0, 0, 65536.0, 1.0, None,
+                                      None) == zb.ZERO_EINVAL                                 # t = 0

@@ -191,3 +191,101 @@ def test_apply_is_profiled_unchained(env):
         zb.zero_profile_enable(0)
     say("apply profile", p.steps, p.stats_ms, p.update_ms)
     assert p.steps == 3 and p.update_ms > 0 and p.stats_ms < p.update_ms
+
+
+def _ranks_async(env, psi, nd, g16, theta, m, v, t, scale, clip, wd=0.01, inject=None):
+    """Asynchronous split phase over N_d emulated ranks: local sums into device memory, a
+    rank-ordered fp64 sum on the device, the update reading it; returns (buffers, flags)."""
+    torch, zb, dev = env
+    S, _, _, padded = oracle.layout(psi, nd, 0)
+    bufs = _flat(env, psi, padded, g16, theta, m, v)
+    shards = [zb.zero_partition_layout(psi, nd, r) for r in range(nd)]
+    local = torch.zeros(nd, dtype=torch.float64, device=dev)
+    for r, l in enumerate(shards):
+        zb.zero_shard_stats_async(bufs[0].view[l.offset:l.offset + l.valid_numel], local[r:r + 1])
+    glob = local[0:1].clone()
+    for r in range(1, nd):  # the device-side exchange: every rank adds the same values in rank order
+        glob = glob + local[r:r + 1]
+    if inject is not None:
+        glob.fill_(inject)
+    flags = torch.full((nd,), -1, dtype=torch.int32, device=dev)
+    for r, l in enumerate(shards):
+        sl = slice(l.offset, l.offset + l.valid_numel)
+        zb.zero_shard_apply_async(*(b.view[sl] for b in bufs), glob, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
+                                  wd, t, scale, clip, skipped=flags[r:r + 1])
+    return bufs, flags, local, glob
+
+
+@pytest.mark.parametrize("psi,nd", [(4_194_305, 4), (1_000_003, 7)])
+def test_async_split_equals_sync_split_and_oracle(env, psi, nd):
+    torch, zb, dev = env
+    w = workloads.WORKLOADS["tiny"]
+    theta, m, v = workloads.initial_state(w, psi)
+    m += np.float32(1e-5)
+    v += np.float32(1e-9)
+    g16 = workloads.gradients(w, psi, 1, w.loss_scale)
+    say("async split psi", psi, "nd", nd)
+    a_bufs, flags, local, glob = _ranks_async(env, psi, nd, g16, theta, m, v, 1, w.loss_scale, w.clip)
+    # the synchronous split phase from the same inputs
+    S, _, _, padded = oracle.layout(psi, nd, 0)
+    s_bufs = _flat(env, psi, padded, g16, theta, m, v)
+    shards = [zb.zero_partition_layout(psi, nd, r) for r in range(nd)]
+    host_local = [zb.zero_shard_stats(s_bufs[0].view[l.offset:l.offset + l.valid_numel]) for l in shards]
+    g = 0.0
+    for x in host_local:
+        g += x
+    for l in shards:
+        sl = slice(l.offset, l.offset + l.valid_numel)
+        assert zb.zero_shard_apply(*(b.view[sl] for b in s_bufs), g, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
+                                   0.01, 1, w.loss_scale, w.clip) == 0
+    torch.cuda.synchronize()
+    assert flags.cpu().tolist() == [0] * nd
+    assert local.cpu().tolist() == host_local and float(glob.item()) == g
+    for x, y in zip(a_bufs[1:], s_bufs[1:]):
+        assert np.array_equal(x.download().view(np.uint8), y.download().view(np.uint8))
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(psi)]
+    skip, sc = H.oracle_step(g16, *ref, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], 0.01, 1, w.loss_scale, w.clip)
+    assert skip == 0 and abs(g / sc.sumsq - 1) <= 1e-12
+    d = H.compare_state([b.download()[:psi] for b in a_bufs[1:]], ref)
+    assert all(b.guards_intact() for b in a_bufs + s_bufs)
+    say("async split", d)
+
+
+@pytest.mark.parametrize("inject", [None, float("inf"), float("nan"), -1.0])
+def test_async_split_skips_without_writing(env, inject):
+    torch, zb, dev = env
+    w = workloads.WORKLOADS["tiny"]
+    psi, nd = 400_003, 4
+    theta, m, v = workloads.initial_state(w, psi)
+    g16 = workloads.gradients(w, psi, 1, w.loss_scale)
+    if inject is None:
+        g16[oracle.layout(psi, nd, 2)[1] + 17] = 0x7C00  # an inf gradient on rank 2
+    bufs, flags, local, glob = _ranks_async(env, psi, nd, g16, theta, m, v, 1, w.loss_scale, w.clip, inject=inject)
+    torch.cuda.synchronize()
+    assert flags.cpu().tolist() == [1] * nd
+    if inject is None:
+        assert [np.isfinite(x) for x in local.cpu().tolist()] == [True, True, False, True]
+    assert np.array_equal(bufs[1].download()[:psi], theta) and np.array_equal(bufs[2].download()[:psi], m)
+    assert np.all(bufs[4].download() == workloads.P16_SENTINEL)
+
+
+def test_async_flag_into_mapped_host_memory(env):
+    torch, zb, dev = env
+    n = 100_003
+    g16, theta, m, v = workloads.random_case(203, n)
+    bufs = [H.Guarded(torch, n, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                                  torch.float16)]
+    for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    d_sum = torch.empty(1, dtype=torch.float64, device=dev)
+    flag = torch.full((1,), -1, dtype=torch.int32, pin_memory=True)
+    zb.zero_shard_stats_async(bufs[0].view, d_sum)
+    zb.zero_shard_apply_async(*(b.view for b in bufs), d_sum, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
+                              HP["weight_decay"], 1, 2.0 ** 16, 1.0, skipped=flag.data_ptr())
+    torch.cuda.current_stream().synchronize()
+    assert int(flag[0]) == 0
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)]
+    skip, _ = H.oracle_step(g16, *ref, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], HP["weight_decay"], 1, 2.0 ** 16,
+                            1.0)
+    assert skip == 0
+    say("async mapped flag", H.compare_state([b.download() for b in bufs[1:]], ref))
