@@ -240,3 +240,36 @@ def test_async_split_rejects_without_a_gpu(zb):
     assert lib.zero_shard_apply_async(*G, 10, G[1] + 8, *hp, None, None) == zb.ZERO_EINVAL  # sum inside master
     assert lib.zero_shard_apply_async(*G, 10, 0x60000000, 1e-3, 0.9, 0.999, 1e-8, 0.0, 0, 65536.0, 1.0, None,
                                       None) == zb.ZERO_EINVAL                                 # t = 0
+
+
+def test_header_is_plain_c_and_links_from_c(zb, tmp_path):
+    # The boundary is a C ABI: the header compiles as strict C99, a C program links every
+    # declared entry point against the library and runs the host-only ones.
+    import shutil
+    if shutil.which("gcc") is None:
+        pytest.skip("needs gcc")
+    names = _declared()
+    src = ["#include \"zero_shard.h\"", "#include <stdio.h>", "int main(void) {",
+           "    typedef void (*fn_t)(void);",
+           "    const fn_t f[] = {" + ", ".join("(fn_t)%s" % n for n in names) + "};",
+           "    zero_layout_t lay; zero_scaler_t sc; double b = 0.0;",
+           "    int rc = zero_partition_layout(62500000000LL, 1024, 1023, &lay);",
+           "    rc |= zero_model_state_bytes(7.5e9, 64, ZERO_STAGE_OS_G, 12.0, &b);",
+           "    rc |= zero_scaler_init(&sc, 65536.0, 1000, 1.0) | zero_scaler_update(&sc, 1);",
+           "    if (zero_partition_layout(10, 0, 0, &lay) != ZERO_EINVAL || zero_last_error()[0] == 0) return 9;",
+           "    zero_partition_layout(62500000000LL, 1024, 1023, &lay);",
+           "    printf(\"%d %lld %lld %lld %lld %.1f %.1f %d\\n\", rc, (long long)lay.shard_numel, (long long)lay.offset,",
+           "           (long long)lay.valid_numel, (long long)lay.padded_total, b, sc.scale, (int)(sizeof f / sizeof f[0]));",
+           "    return rc;", "}"]
+    c = tmp_path / "abi.c"
+    c.write_text("\n".join(src) + "\n")
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(zb.LIB_PATH)
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+                    "-I", os.path.join(ROOT, "include"), str(c), "-L", libdir, "-lzeroshard",
+                    "-Wl,-rpath," + libdir, "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], stdout=subprocess.PIPE, check=True).stdout.decode().split()
+    S, off, valid, padded = oracle.layout(62_500_000_000, 1024, 1023)
+    assert out[:5] == ["0", str(S), str(off), str(valid), str(padded)]
+    assert float(out[5]) == pytest.approx(oracle.model_state_bytes(7.5e9, 64, oracle.STAGE_OS_G))
+    assert float(out[6]) == 32768.0 and int(out[7]) == len(names)
