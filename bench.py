@@ -173,6 +173,9 @@ def main():
     ap.add_argument("--split-phase", action="store_true",
                     help="adam only: each step as zero_shard_stats -> (one rank: the local sum is the global one) "
                          "-> zero_shard_apply, the seam a multi-rank run exchanges 8 bytes at")
+    ap.add_argument("--resident", choices=("eager", "graph"), default=None,
+                    help="adam only: the resident step (state record and loss scaler on the device, no host "
+                         "wait), called eagerly or replayed from a captured HIP graph")
     ap.add_argument("--async-seam", action="store_true",
                     help="with --split-phase: the asynchronous calls (sums in device memory, no host wait; the "
                          "skip flags are checked after the timed region)")
@@ -226,9 +229,41 @@ def main():
     d_sum = torch.zeros(1, dtype=torch.float64, device=dev)
     d_flags = torch.full((args.warmup + args.steps,), -1, dtype=torch.int32, device=dev)
     calls = [0]
+    if args.resident and (lamb or args.split_phase):
+        print("bench.py: --resident measures the Adam step alone", file=sys.stderr)
+        sys.exit(2)
+    r_state = graphs = None
+    if args.resident:
+        r_state = zb.resident_state(dev, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, w.clip, w.loss_scale,
+                                    window=1000)
+    if args.resident == "graph":
+        # one graph per gradient buffer, replayed alternately; the capture stream gets its workspace
+        # (and the arrays their checks) from eager calls on a scratch state first
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        scratch = zb.resident_state(dev, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, w.clip, w.loss_scale)
+        with torch.cuda.stream(cap):
+            for d_g in d_gs:
+                zb.zero_shard_step_resident(d_g, d_theta, d_m, d_v, d_p, scratch)
+        cap.synchronize()
+        graphs = []
+        for d_g in d_gs:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=cap):
+                zb.zero_shard_step_resident(d_g, d_theta, d_m, d_v, d_p, r_state)
+            graphs.append(gr)
+        torch.cuda.synchronize()
 
     def step():
         d_g = d_gs[scaler.t_next % 2]
+        if args.resident == "graph":
+            graphs[scaler.t_next % 2].replay()
+            scaler.update(False)   # the device record keeps the real schedule; checked after timing
+            return 0
+        if args.resident == "eager":
+            zb.zero_shard_step_resident(d_g, d_theta, d_m, d_v, d_p, r_state, stream=stream)
+            scaler.update(False)
+            return 0
         if args.async_seam:
             # one rank: the local sum in device memory is the global one; no host wait, so the
             # flag is read after the timed region and t advances as if every step applied
@@ -291,8 +326,20 @@ def main():
     zb.zero_profile_enable(False)
     prof = zb.zero_profile_read()
     lprof = zb.zero_lamb_profile_read()
+    if args.resident == "graph":
+        # replays record no events: the kernels' times come from eager resident steps (the same
+        # kernels on the same buffers), on a scratch state record
+        zb.zero_profile_enable(1)
+        for k in range(20):
+            zb.zero_shard_step_resident(d_gs[k % 2], d_theta, d_m, d_v, d_p, scratch, stream=stream)
+        torch.cuda.synchronize()
+        zb.zero_profile_enable(False)
+        prof = zb.zero_profile_read()
     if args.async_seam:
         skips = int((d_flags != 0).sum().item())
+    if args.resident:
+        rs = zb.read_resident_state(r_state)
+        skips = int(rs.steps - (rs.t - 1))
     if skips:
         print("bench.py: %d timed steps skipped on overflow; the measurement is invalid" % skips, file=sys.stderr)
         sys.exit(1)
@@ -336,6 +383,10 @@ def main():
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
     }
+    if args.resident:
+        out["config"].update(path="resident step (device state record and loss scaler, no host wait)" +
+                             (", replayed from captured HIP graphs; kernel_ms from 20 eager resident steps"
+                              if args.resident == "graph" else ", eager calls"))
     if args.split_phase:
         out["config"].update(path="split phase: zero_shard_stats_async, device-resident global sum, "
                                   "zero_shard_apply_async (no host wait)" if args.async_seam else

@@ -165,6 +165,42 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
                            double weight_decay, int64_t step, double loss_scale, double clip, int32_t* skipped,
                            void* stream);
 
+/* Resident step: the whole step, loss scaler included, driven by a state
+ * record in DEVICE memory, so a call only enqueues kernels and never waits;
+ * the enqueued work can be captured into a HIP graph and replayed, each replay
+ * being the next optimizer step.  The caller owns the record: it writes the
+ * hyperparameters and the scaler's starting values (host copy before the
+ * first step, or between steps), and reads t / loss_scale / skipped whenever
+ * it needs them.  Per step, on the device:
+ *   statistics of grad16 (as zero_shard_step) -> scalars from the record's
+ *   loss_scale and clip -> the fp32 constants from lr, betas, eps, weight
+ *   decay and t (each computed in double and rounded once, the bias
+ *   corrections with the device's pow) -> skip or the update -> the scaler:
+ *   on a skip halve loss_scale (not below min_scale), good = 0; else t += 1,
+ *   good += 1 and double loss_scale when good reaches window (> 0), good = 0.
+ * Same arrays, checks and skip semantics as zero_shard_step.  The first call
+ * on a stream allocates the stream's workspace, so make one call before
+ * capturing; while the stream is capturing, the allocation checks and the
+ * sampled timing (zero_profile_enable) are left out, so make an eager call
+ * with the same arrays first.  `state` must be 8-byte aligned device memory
+ * (or mapped host memory) that no array overlaps; its hyperparameters are the
+ * caller's to keep in the ranges zero_shard_step accepts (the kernels do not
+ * check them). */
+typedef struct {
+    double lr, beta1, beta2, eps, weight_decay, clip; /* hyperparameters (caller)          */
+    double loss_scale;                                /* current loss scale                */
+    double min_scale;                                 /* floor of the halving               */
+    int64_t window;                                   /* growth window; <= 0: never grow    */
+    int64_t t;                                        /* t of the next applied update, >= 1 */
+    int64_t good;                                     /* applied steps since skip or growth */
+    int64_t steps;                                    /* steps taken, applied or skipped    */
+    int32_t skipped;                                  /* decision of the last step          */
+    int32_t pad_;
+} zero_resident_state_t;
+
+int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32, float* v32,
+                             uint16_t* param16_out, int64_t n, zero_resident_state_t* state, void* stream);
+
 /* The array checks of zero_shard_step without launching anything: n range,
  * NULL pointers, alignment, that each array [p, p + n*size) lies inside one
  * GPU-accessible allocation (hipMemGetAddressRange), then overlap.

@@ -45,6 +45,14 @@ class Profile(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("update_ms", ctypes.c_double)]
 
 
+class ResidentState(ctypes.Structure):
+    """Mirror of zero_resident_state_t (the resident step's device record)."""
+    _fields_ = [(k, ctypes.c_double) for k in ("lr", "beta1", "beta2", "eps", "weight_decay", "clip", "loss_scale",
+                                               "min_scale")] + \
+               [(k, ctypes.c_int64) for k in ("window", "t", "good", "steps")] + \
+               [("skipped", ctypes.c_int32), ("pad_", ctypes.c_int32)]
+
+
 class LambProfile(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("moments_ms", ctypes.c_double),
                 ("layer_ms", ctypes.c_double), ("apply_ms", ctypes.c_double)]
@@ -68,6 +76,7 @@ _lib.zero_probe_copy.argtypes = [_P, _P, _i64, _P]
 _lib.zero_shard_stats_async.argtypes = [_P, _i64, _P, _P]
 _lib.zero_shard_apply_async.argtypes = [_P, _P, _P, _P, _P, _i64, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl,
                                         _P, _P]
+_lib.zero_shard_step_resident.argtypes = [_P, _P, _P, _P, _P, _i64, _P, _P]
 _lib.zero_lamb_plan_create.argtypes = [_P, _i32, _i64, ctypes.POINTER(_P)]
 _lib.zero_lamb_plan_destroy.argtypes = [_P]
 _lib.zero_lamb_step.argtypes = [_P, _P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _dbl, _dbl, _P]
@@ -79,7 +88,7 @@ for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
            "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step",
            "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async",
-           "zero_shard_apply_async"):
+           "zero_shard_apply_async", "zero_shard_step_resident"):
     getattr(_lib, _f).restype = ctypes.c_int
 
 EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
@@ -87,7 +96,7 @@ EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
            "zero_profile_read", "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy",
            "zero_lamb_step", "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read",
-           "zero_shard_stats_async", "zero_shard_apply_async")
+           "zero_shard_stats_async", "zero_shard_apply_async", "zero_shard_step_resident")
 
 
 def _check(rc):
@@ -205,6 +214,40 @@ def zero_shard_apply_async(grad16, master32, m32, v32, param16_out, global_sumsq
         _addr(global_sumsq, (torch.float64,), "global_sumsq"), float(lr), float(beta1), float(beta2), float(eps),
         float(weight_decay), int(step), float(loss_scale), float(clip),
         _addr(skipped, (torch.int32,), "skipped"), _stream(stream)))
+
+
+def resident_state(device, lr, beta1, beta2, eps, weight_decay, clip, loss_scale, min_scale=1.0, window=1000, t=1):
+    """A zero_resident_state_t record in device memory (a uint8 torch tensor), initialised
+    from the host."""
+    import torch
+    st = ResidentState(lr=lr, beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay, clip=clip,
+                       loss_scale=loss_scale, min_scale=min_scale, window=window, t=t, good=0, steps=0, skipped=0)
+    host = torch.frombuffer(bytearray(bytes(st)), dtype=torch.uint8)
+    return host.to(device)
+
+
+def read_resident_state(state_tensor) -> ResidentState:
+    """The record's current contents (copies to the host: synchronises with its stream)."""
+    return ResidentState.from_buffer_copy(bytes(state_tensor.cpu().numpy().tobytes()))
+
+
+def zero_shard_step_resident(grad16, master32, m32, v32, param16_out, state, n=None, stream=None):
+    """Enqueue one resident step (no host wait; capturable).  `state` is the device record
+    from resident_state() or a raw device address."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    if n is None:
+        n = grad16.numel()
+        for t in (master32, m32, v32, param16_out):
+            if t.numel() != n:
+                raise ValueError("shard tensors differ in length")
+    if not isinstance(state, int) and state.numel() * state.element_size() < ctypes.sizeof(ResidentState):
+        raise ValueError("state must hold a zero_resident_state_t (%d bytes)" % ctypes.sizeof(ResidentState))
+    _check(_lib.zero_shard_step_resident(
+        _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), _addr(state, None, "state"),
+        _stream(stream)))
 
 
 def zero_shard_validate(grad16, master32, m32, v32, param16_out, n):

@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "zero_shard.h"
+
 namespace zs {
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -284,6 +286,50 @@ constexpr int kFinalBlock = 256;
     }
 }
 
+// Resident step, before the update: the result record from the statistics total
+// and the record's loss scale and clip, and the fp32 constants from the
+// record's hyperparameters and t (each computed in double and rounded once).
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_resident_prepare(
+    const double* __restrict__ sumsq, const zero_resident_state_t* __restrict__ st, Result* __restrict__ res,
+    AdamConst* __restrict__ cout, uint32_t seq) {
+    if (threadIdx.x == 0) {
+        *res = make_result(*sumsq, st->loss_scale, st->clip, seq);
+        const double t = (double)st->t;
+        AdamConst c;
+        c.lr = (float)st->lr;
+        c.b1 = (float)st->beta1;
+        c.omb1 = (float)(1.0 - st->beta1);
+        c.b2 = (float)st->beta2;
+        c.omb2 = (float)(1.0 - st->beta2);
+        c.bc1 = (float)(1.0 - pow(st->beta1, t));
+        c.bc2 = (float)(1.0 - pow(st->beta2, t));
+        c.eps = (float)st->eps;
+        c.wd = (float)st->weight_decay;
+        *cout = c;
+    }
+}
+
+// Resident step, after the update: the loss-scale schedule on the device.
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_resident_finish(zero_resident_state_t* __restrict__ st,
+                                                                                 const Result* __restrict__ res) {
+    if (threadIdx.x == 0) {
+        st->steps += 1;
+        st->skipped = res->skip;
+        if (res->skip) {
+            const double h = st->loss_scale * 0.5;
+            st->loss_scale = h > st->min_scale ? h : st->min_scale;
+            st->good = 0;
+        } else {
+            st->t += 1;
+            st->good += 1;
+            if (st->window > 0 && st->good >= st->window) {
+                st->loss_scale *= 2.0;
+                st->good = 0;
+            }
+        }
+    }
+}
+
 // Result record from a global sum of squares supplied by the caller (the
 // split-phase step: each rank's local sums combined outside the library).
 [[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_result(Result* __restrict__ res,
@@ -331,14 +377,18 @@ __device__ __forceinline__ void adam_one(const uint16_t* g, float* th, float* m,
 // consecutive vectors.  A tile is BLOCK*U vectors; each thread loads its U
 // vectors of all four inputs before computing.  Elements [head + 4*nvec, n)
 // are the tail (0..3).  Any grid size is valid (tiles are strided by it).
+// The fp32 constants come by value, or from device memory when cdev is not
+// NULL (the resident step computes them on the device).
 template <int BLOCK, int U, bool NTL, bool NTS, bool XCD, bool REV>
 __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__ g, float* __restrict__ th,
                                                     float* __restrict__ m, float* __restrict__ v,
                                                     uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec,
-                                                    const Result* __restrict__ res, AdamConst c) {
+                                                    const Result* __restrict__ res, AdamConst c_arg,
+                                                    const AdamConst* __restrict__ cdev) {
     if (res->skip)
         return;
     const float mult = res->mult;
+    const AdamConst c = cdev ? *cdev : c_arg;
     if (blockIdx.x == 0 && threadIdx.x < 8) {
         const int64_t t = threadIdx.x;
         const int64_t i = t < 4 ? t : head + 4 * nvec + (t - 4);
@@ -394,10 +444,12 @@ __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__
 // K2 (scalar path) for arrays whose element misalignments differ.
 [[maybe_unused]] static __global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
     const uint16_t* __restrict__ g, float* __restrict__ th, float* __restrict__ m, float* __restrict__ v,
-    uint16_t* __restrict__ p, int64_t n, const Result* __restrict__ res, AdamConst c) {
+    uint16_t* __restrict__ p, int64_t n, const Result* __restrict__ res, AdamConst c_arg,
+    const AdamConst* __restrict__ cdev) {
     if (res->skip)
         return;
     const float mult = res->mult;
+    const AdamConst c = cdev ? *cdev : c_arg;
     const int64_t stride = (int64_t)gridDim.x * kScalarBlock;
     for (int64_t i = (int64_t)blockIdx.x * kScalarBlock + threadIdx.x; i < n; i += stride)
         adam_one(g, th, m, v, p, i, mult, c);

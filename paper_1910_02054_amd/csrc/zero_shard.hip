@@ -170,12 +170,16 @@ int get_ctx(hipStream_t stream, Ctx** out) {
         kAdamBlock, kAdamPerCU, prop, &c->adam_resident);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->dsum), sizeof(double)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->dconst), sizeof(zs::AdamConst)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
               hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess;
     if (!ok) {
         if (c->part) (void)hipFree(c->part);
         if (c->res) (void)hipFree(c->res);
+        if (c->dsum) (void)hipFree(c->dsum);
+        if (c->dconst) (void)hipFree(c->dconst);
         if (c->host) (void)hipHostFree(c->host);
         (void)hipGetLastError();
         return fail(ZERO_ENOMEM, "could not allocate the step workspace on device %d", dev);
@@ -405,16 +409,18 @@ int prof_every() {
     return g_prof_every;
 }
 
-// The fused update reading its scalars from ctx->res.
+// The fused update reading its scalars from ctx->res; the fp32 constants are
+// `c`, or the device copy at cdev when it is not NULL.
 int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
-                  int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream) {
+                  int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream,
+                  const zs::AdamConst* cdev = nullptr) {
     if (pl.vec)
         zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>
             <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
-                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c);
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c, cdev);
     else
         zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
-            grad16, master32, m32, v32, param16_out, n, ctx->res, c);
+            grad16, master32, m32, v32, param16_out, n, ctx->res, c, cdev);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
@@ -796,6 +802,75 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
         if ((rc = prof_end(ctx, pr)))
             return rc;
     }
+    return ZERO_OK;
+}
+
+int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                             int64_t n, zero_resident_state_t* state, void* stream_) {
+    const char* fn = "zero_shard_step_resident";
+    int rc = check_arrays(fn, grad16, master32, m32, v32, param16_out, n);
+    if (rc)
+        return rc;
+    if (!state || reinterpret_cast<uintptr_t>(state) % 8)
+        return fail(ZERO_EINVAL, "%s: state must be an 8-byte aligned device pointer", fn);
+    {
+        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
+                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
+                                reinterpret_cast<uintptr_t>(param16_out)};
+        const size_t esz[5] = {2, 4, 4, 4, 2};
+        for (int i = 0; i < 5 && n > 0; ++i)
+            if (overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(state), sizeof *state))
+                return fail(ZERO_EINVAL, "%s: state overlaps array %d", fn, i);
+    }
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    Ctx* ctx = nullptr;
+    if ((rc = get_ctx(stream, &ctx)))
+        return rc;
+    std::lock_guard<std::mutex> lk(ctx->mu);
+    // While the stream is being captured into a graph only kernel launches are
+    // recorded: the allocation lookups and the sampled timing run on eager calls.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    HIP_TRY(hipStreamIsCapturing(stream, &cap));
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (!capturing) {
+        const void* ptr = state;
+        const size_t bytes = sizeof *state;
+        if ((rc = check_ranges(fn, &ptr, &bytes, 1)))
+            return rc;
+        if (n > 0 && (rc = check_shard_ranges_cached(ctx, fn, grad16, master32, m32, v32, param16_out, n)))
+            return rc;
+    }
+    const uint32_t seq = next_seq(ctx);
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    ProfRec pr{};
+    const bool prof = !capturing && n > 0 && prof_begin(ctx, &pr, false);
+    if (prof && !pr.end)
+        return fail(ZERO_EHIP, "%s: could not create a profiling event", fn);
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.start, stream));
+    if (n > 0) {
+        zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
+            <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+        HIP_TRY(hipGetLastError());
+        zs::k_finalize_sum<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->dsum);
+    } else {
+        zs::k_set_value<<<1, 64, 0, stream>>>(ctx->dsum, 0.0);
+    }
+    HIP_TRY(hipGetLastError());
+    zs::k_resident_prepare<<<1, 64, 0, stream>>>(ctx->dsum, state, ctx->res, ctx->dconst, seq);
+    HIP_TRY(hipGetLastError());
+    if (prof)
+        HIP_TRY(hipEventRecord(pr.mid, stream));
+    if (n > 0 && (rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, zs::AdamConst{}, stream,
+                                     ctx->dconst)))
+        return rc;
+    if (prof) {
+        HIP_TRY(hipEventRecord(pr.end, stream));
+        if ((rc = prof_end(ctx, pr)))
+            return rc;
+    }
+    zs::k_resident_finish<<<1, 64, 0, stream>>>(state, ctx->res);
+    HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
 

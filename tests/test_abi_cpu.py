@@ -273,3 +273,31 @@ def test_header_is_plain_c_and_links_from_c(zb, tmp_path):
     assert out[:5] == ["0", str(S), str(off), str(valid), str(padded)]
     assert float(out[5]) == pytest.approx(oracle.model_state_bytes(7.5e9, 64, oracle.STAGE_OS_G))
     assert float(out[6]) == 32768.0 and int(out[7]) == len(names)
+
+
+def test_binding_structs_match_the_c_layout(zb, tmp_path):
+    # every struct the binding mirrors has the header's size and field offsets
+    import shutil
+    if shutil.which("gcc") is None:
+        pytest.skip("needs gcc")
+    pairs = [("zero_layout_t", zb.Layout), ("zero_step_stats_t", zb.StepStats), ("zero_scaler_t", zb.ScalerState),
+             ("zero_profile_t", zb.Profile), ("zero_lamb_profile_t", zb.LambProfile),
+             ("zero_resident_state_t", zb.ResidentState)]
+    text = open(HEADER).read()
+    lines = ["#include \"zero_shard.h\"", "#include <stdio.h>", "#include <stddef.h>", "int main(void) {"]
+    expect = []
+    for cname, py in pairs:
+        assert cname in text, cname
+        lines.append('    printf("%%zu\\n", sizeof(%s));' % cname)
+        expect.append(ctypes.sizeof(py))
+        for fname, _ in py._fields_:
+            lines.append('    printf("%%zu\\n", offsetof(%s, %s));' % (cname, fname))
+            expect.append(getattr(py, fname).offset)
+    lines += ["    return 0;", "}"]
+    c = tmp_path / "layout.c"
+    c.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), str(c), "-o",
+                    str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], stdout=subprocess.PIPE, check=True).stdout.split()]
+    assert got == expect
