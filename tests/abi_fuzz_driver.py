@@ -87,4 +87,9 @@ for _ in range(2000):
     L.zero_shard_apply_async(*G, r.choice([-1, 10]), r.choice([None, 0x60000004]), 1e-3, 0.9, 0.999, 1e-8, 0.0,
                              r.choice([0, -1]), 65536.0, 1.0, r.choice([None, 0x70000002]), None)
     L.zero_last_error()
+L.zero_shard_step_resident.argtypes = [P, P, P, P, P, i64, P, P]
+for _ in range(2000):
+    ptrs = [p + r.choice([0, 1]) for p in G]
+    L.zero_shard_step_resident(*ptrs, r.choice([-1, 10, 1 << 41]), r.choice([None, 0x60000004, G[1] + 8]), None)
+    L.zero_last_error()
 print("driver done", bad, "rejected or empty calls")

@@ -301,3 +301,14 @@ def test_binding_structs_match_the_c_layout(zb, tmp_path):
                     str(exe)], check=True)
     got = [int(x) for x in subprocess.run([str(exe)], stdout=subprocess.PIPE, check=True).stdout.split()]
     assert got == expect
+
+
+def test_resident_step_rejects_without_a_gpu(zb):
+    lib = zb.raw_library()
+    G = [0x10000000, 0x20000000, 0x30000000, 0x40000000, 0x50000000]
+    assert lib.zero_shard_step_resident(*G, 10, None, None) == zb.ZERO_EINVAL           # NULL state
+    assert lib.zero_shard_step_resident(*G, 10, 0x60000004, None) == zb.ZERO_EINVAL     # misaligned state
+    assert lib.zero_shard_step_resident(*G, 10, G[1] + 8, None) == zb.ZERO_EINVAL       # state inside master
+    assert lib.zero_shard_step_resident(G[0] + 1, *G[1:], 10, 0x60000000, None) == zb.ZERO_EINVAL
+    assert lib.zero_shard_step_resident(*G, -1, 0x60000000, None) == zb.ZERO_EINVAL
+    assert "state" in zb.zero_last_error() or "n=" in zb.zero_last_error()
