@@ -377,9 +377,9 @@ __device__ __forceinline__ void adam_one(const uint16_t* g, float* th, float* m,
 // consecutive vectors.  A tile is BLOCK*U vectors; each thread loads its U
 // vectors of all four inputs before computing.  Elements [head + 4*nvec, n)
 // are the tail (0..3).  Any grid size is valid (tiles are strided by it).
-// The fp32 constants come by value, or from device memory when cdev is not
-// NULL (the resident step computes them on the device).
-template <int BLOCK, int U, bool NTL, bool NTS, bool XCD, bool REV>
+// The fp32 constants come by value, or with CDEV from device memory (the
+// resident step computes them on the device).
+template <int BLOCK, int U, bool NTL, bool NTS, bool XCD, bool REV, bool CDEV>
 __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__ g, float* __restrict__ th,
                                                     float* __restrict__ m, float* __restrict__ v,
                                                     uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec,
@@ -388,7 +388,9 @@ __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__
     if (res->skip)
         return;
     const float mult = res->mult;
-    const AdamConst c = cdev ? *cdev : c_arg;
+    AdamConst c = c_arg;
+    if constexpr (CDEV)
+        c = *cdev;
     if (blockIdx.x == 0 && threadIdx.x < 8) {
         const int64_t t = threadIdx.x;
         const int64_t i = t < 4 ? t : head + 4 * nvec + (t - 4);
@@ -442,14 +444,17 @@ __global__ __launch_bounds__(BLOCK) void k_adam_vec(const uint16_t* __restrict__
 }
 
 // K2 (scalar path) for arrays whose element misalignments differ.
-[[maybe_unused]] static __global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
+template <bool CDEV>
+__global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
     const uint16_t* __restrict__ g, float* __restrict__ th, float* __restrict__ m, float* __restrict__ v,
     uint16_t* __restrict__ p, int64_t n, const Result* __restrict__ res, AdamConst c_arg,
     const AdamConst* __restrict__ cdev) {
     if (res->skip)
         return;
     const float mult = res->mult;
-    const AdamConst c = cdev ? *cdev : c_arg;
+    AdamConst c = c_arg;
+    if constexpr (CDEV)
+        c = *cdev;
     const int64_t stride = (int64_t)gridDim.x * kScalarBlock;
     for (int64_t i = (int64_t)blockIdx.x * kScalarBlock + threadIdx.x; i < n; i += stride)
         adam_one(g, th, m, v, p, i, mult, c);

@@ -166,7 +166,8 @@ int get_ctx(hipStream_t stream, Ctx** out) {
         reinterpret_cast<const void*>(zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>), kStatsBlock,
         kStatsPerCU, prop, &c->stats_resident);
     c->adam_lds = occupancy_lds(
-        reinterpret_cast<const void*>(zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>),
+        reinterpret_cast<const void*>(
+            zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>),
         kAdamBlock, kAdamPerCU, prop, &c->adam_resident);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
@@ -414,13 +415,20 @@ int prof_every() {
 int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
                   int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream,
                   const zs::AdamConst* cdev = nullptr) {
-    if (pl.vec)
-        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV>
+    if (pl.vec && cdev)
+        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, true>
             <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
                 grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c, cdev);
-    else
-        zs::k_adam_scalar<<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
+    else if (pl.vec)
+        zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>
+            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c, nullptr);
+    else if (cdev)
+        zs::k_adam_scalar<true><<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
             grad16, master32, m32, v32, param16_out, n, ctx->res, c, cdev);
+    else
+        zs::k_adam_scalar<false><<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
+            grad16, master32, m32, v32, param16_out, n, ctx->res, c, nullptr);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
