@@ -18,6 +18,13 @@
 //               device memory and to a host-mapped record.
 //   k_adam_*    the fused update: unscale+clip, Adam with bias correction, fp16
 //               cast; 14 bytes read and 14 bytes written per element.
+// The other ways of running the same step swap only the one-thread kernels
+// around these: the split phase takes the global sum from the host
+// (k_set_result) or from device memory (k_finalize_sum writes a rank's local
+// sum, k_set_result_dev reads the combined one); the resident step derives the
+// scalars and the fp32 constants from a state record in device memory
+// (k_resident_prepare) and runs the loss-scale schedule there
+// (k_resident_finish).
 //
 // Numerics: every fp32 operation of the update is correctly rounded (IEEE
 // division and square root, no contraction), in the order Adam's bias-corrected
