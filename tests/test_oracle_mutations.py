@@ -19,7 +19,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "zero_oracle.c")
 PIN_TESTS = ["tests/test_oracle_accounting.py", "tests/test_oracle_layout.py", "tests/test_oracle_binary16.py",
              "tests/test_oracle_stats.py", "tests/test_oracle_adam.py", "tests/test_oracle_invariants.py",
-             "tests/test_oracle_lamb.py"]
+             "tests/test_oracle_lamb.py", "tests/test_oracle_scaler.py"]
 
 MUTANTS = {
     "update_sign": ("float th = theta[i] - h->lr * u;", "float th = theta[i] + h->lr * u;"),
@@ -47,6 +47,8 @@ MUTANTS = {
     "writes_on_skip": ("    if (sc.skip)\n        return 1;\n", ""),
     "scaler_no_halving": ("double s = *scale / 2.0;", "double s = *scale;"),
     "t_counts_skips": ("        *good = 0;\n        return;\n", "        *good = 0;\n        *applied += 1;\n        return;\n"),
+    "scaler_growth_late": ("*good >= window", "*good > window"),
+    "scaler_skip_keeps_good": ("        *good = 0;\n        return;\n", "        return;\n"),
     # exact fp32 sum of squares
     "acc_drops_carry": ("        if (i - q >= 1 && carry == 0)\n", "        if (i - q >= 1)\n"),
     "acc_carry_not_added": ("zo_u128 s = (zo_u128)a->limb[i] + carry + (i - q < 2 ? parts[i - q] : 0);",
