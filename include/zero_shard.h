@@ -377,7 +377,8 @@ int zero_profile_read(zero_profile_t* out);
 /* Device-to-device copy of `bytes` bytes with the library's own streaming
  * kernel (16-byte vectors): the achievable-bandwidth reference for the update
  * kernel and the calibration kernel for hardware byte counters.  src and dst
- * must be 16-byte aligned, bytes a multiple of 16, ranges disjoint. */
+ * must be 16-byte aligned, bytes a multiple of 16, ranges disjoint, each inside
+ * one GPU-accessible allocation; ZERO_EINVAL otherwise, before any launch. */
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
 #ifdef __cplusplus

@@ -928,6 +928,13 @@ int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {
         return fail(ZERO_EINVAL, "zero_probe_copy: ranges overlap");
     if (bytes == 0)
         return ZERO_OK;
+    {
+        const void* ptrs[2] = {src, dst};
+        const size_t sizes[2] = {(size_t)bytes, (size_t)bytes};
+        int rc = check_ranges("zero_probe_copy", ptrs, sizes, 2);
+        if (rc)
+            return rc;
+    }
     const int64_t nvec = bytes / 16;
     int64_t blocks = ceil_div(nvec, (int64_t)kCopyBlock * kCopyUnroll);
     blocks = blocks < 1 ? 1 : (blocks > kAdamMaxBlocks ? kAdamMaxBlocks : blocks);

@@ -185,6 +185,18 @@ def test_validate_rejects_without_launching(zb):
     assert "GPU-accessible" in zb.zero_last_error()
 
 
+def test_probe_copy_rejects_without_launching(zb):
+    lib = zb.raw_library()
+    lib.zero_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    assert lib.zero_probe_copy(GOOD[1], GOOD[2], 24, None) == zb.ZERO_EINVAL        # not a multiple of 16
+    assert lib.zero_probe_copy(GOOD[1] + 4, GOOD[2], 32, None) == zb.ZERO_EINVAL    # misaligned
+    assert lib.zero_probe_copy(GOOD[1], GOOD[1] + 16, 64, None) == zb.ZERO_EINVAL   # overlap
+    assert lib.zero_probe_copy(GOOD[1], GOOD[2], 0, None) == zb.ZERO_OK
+    # addresses outside any GPU allocation are refused before a launch
+    assert lib.zero_probe_copy(GOOD[1], GOOD[2], 64, None) == zb.ZERO_EINVAL
+    assert "GPU-accessible" in zb.zero_last_error()
+
+
 def test_lamb_plan_rejects_bad_tables_without_a_gpu(zb):
     lib = zb.raw_library()
     out = ctypes.c_void_p()
