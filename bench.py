@@ -109,6 +109,20 @@ def measured_lamb_traffic(n):
     return _traffic_from(LAMB_TRAFFIC_FILE, "moments_bytes_per_launch", lamb_kernel_source_hash(), n)
 
 
+def _host_cpu():
+    """The host's CPU model (from /proc/cpuinfo, if readable) and the cores this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
     """The oracle, as it stands, single-threaded on the same shard, 4M-element chunk by chunk
     (each chunk one oracle step: statistics + update), until about budget_s seconds of CPU
@@ -129,7 +143,7 @@ def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
         pos = 0 if b == n else b
     return {"value": done / t_used, "unit": "params/s", "cores": 1, "kind": "oracle",
             "sample": "%d element-updates of the %d-element shard in 4M-element oracle steps (statistics + "
-                      "update), single thread, %.1f s" % (done, n, t_used)}
+                      "update), single thread, %.1f s" % (done, n, t_used), **_host_cpu()}
 
 
 def lamb_cpu_baseline(w, seg, theta, m, v, g16, scale, budget_s):
@@ -153,7 +167,7 @@ def lamb_cpu_baseline(w, seg, theta, m, v, g16, scale, budget_s):
     return {"value": done / t_used, "unit": "params/s", "cores": 1, "kind": "oracle",
             "sample": "%d element-updates over whole layers of the %d-element shard, one oracle LAMB step per "
                       "layer (statistics + moments + exact layer norms + update), single thread, %.1f s"
-                      % (done, int(seg[-1]), t_used)}
+                      % (done, int(seg[-1]), t_used), **_host_cpu()}
 
 
 def main():
@@ -164,6 +178,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle CPU time")
+    ap.add_argument("--step-samples", type=int, default=50,
+                    help="after the timed region, time this many further steps one by one with HIP events "
+                         "(median, p10, p90 of single steps; 0 = off)")
     ap.add_argument("--profile-every", type=int, default=10,
                     help="time the kernels of one step in this many with HIP events (markers cost GPU time)")
     ap.add_argument("--probe-copy-mib", type=int, default=2048,
@@ -227,7 +244,8 @@ def main():
         print("bench.py: --async-seam needs --split-phase", file=sys.stderr)
         sys.exit(2)
     d_sum = torch.zeros(1, dtype=torch.float64, device=dev)
-    d_flags = torch.full((args.warmup + args.steps,), -1, dtype=torch.int32, device=dev)
+    d_flags = torch.full((args.warmup + args.steps + max(0, args.step_samples),), -1, dtype=torch.int32,
+                         device=dev)
     calls = [0]
     if args.resident and (lamb or args.split_phase):
         print("bench.py: --resident measures the Adam step alone", file=sys.stderr)
@@ -267,6 +285,7 @@ def main():
         if args.async_seam:
             # one rank: the local sum in device memory is the global one; no host wait, so the
             # flag is read after the timed region and t advances as if every step applied
+            assert calls[0] < d_flags.numel(), "more async steps than flag slots"
             zb.zero_shard_stats_async(d_g, d_sum, stream=stream)
             zb.zero_shard_apply_async(d_g, d_theta, d_m, d_v, d_p, d_sum, w.lr, w.beta1, w.beta2, w.eps,
                                       w.weight_decay, scaler.t_next, scaler.scale, w.clip,
@@ -336,7 +355,7 @@ def main():
         zb.zero_profile_enable(False)
         prof = zb.zero_profile_read()
     if args.async_seam:
-        skips = int((d_flags != 0).sum().item())
+        skips = int((d_flags[:calls[0]] != 0).sum().item())
     if args.resident:
         rs = zb.read_resident_state(r_state)
         skips = int(rs.steps - (rs.t - 1))
@@ -346,6 +365,29 @@ def main():
 
     ms = (t1 - t0) * 1e3 / args.steps
     params_per_s = n / (ms * 1e-3)
+    step_q = None
+    if args.step_samples > 0:
+        # single steps, each bracketed by events on its stream (the markers add a few microseconds
+        # of GPU idle per step, so these run a little above ms_per_step of the pipelined region)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.step_samples)]
+        extra_skips = 0
+        for a, b in evs:
+            a.record(stream)
+            extra_skips += step()
+            b.record(stream)
+        torch.cuda.synchronize()
+        if args.async_seam:
+            extra_skips = int((d_flags[:calls[0]] != 0).sum().item())
+        if args.resident:
+            rs = zb.read_resident_state(r_state)
+            extra_skips = int(rs.steps - (rs.t - 1))
+        if extra_skips:
+            print("bench.py: a sampled step skipped on overflow; the samples are invalid", file=sys.stderr)
+            sys.exit(1)
+        qs = np.percentile(np.array([a.elapsed_time(b) for a, b in evs]), [10, 50, 90])
+        step_q = {"p10": float(qs[0]), "p50": float(qs[1]), "p90": float(qs[2]), "steps": args.step_samples,
+                  "timing": "HIP events around each single step on its stream"}
     if lamb:
         step_gbps = LAMB_STEP_BYTES_PER_PARAM * n / (ms * 1e-3) / 1e9
         k = lprof.steps
@@ -379,6 +421,7 @@ def main():
         "hbm_gbps": step_gbps,
         "hbm_frac_of_peak": step_gbps / HBM_PEAK_GBPS,
         "kernel_ms": kernel_ms,
+        "step_ms_quantiles": step_q,
         "roofline": {"bound": "hbm", "kernel": roof_kernel, "achieved": upd_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": upd_gbps / HBM_PEAK_GBPS,
                      "traffic": traffic},
