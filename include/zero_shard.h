@@ -175,9 +175,12 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
  *   statistics of grad16 (as zero_shard_step) -> scalars from the record's
  *   loss_scale and clip -> the fp32 constants from lr, betas, eps, weight
  *   decay and t (each computed in double and rounded once, the bias
- *   corrections with the device's pow) -> skip or the update -> the scaler:
- *   on a skip halve loss_scale (not below min_scale), good = 0; else t += 1,
- *   good += 1 and double loss_scale when good reaches window (> 0), good = 0.
+ *   corrections with the device's pow) -> the scaler: on a skip halve
+ *   loss_scale (not below min_scale), good = 0; else t += 1, good += 1 and
+ *   double loss_scale when good reaches window (> 0), good = 0 -> skip or the
+ *   update.  The record is updated before the update kernel runs (which reads
+ *   only the scalars and constants taken from it before); once the step's work
+ *   on the stream is complete the record describes the step just taken.
  * Same arrays, checks and skip semantics as zero_shard_step.  The first call
  * on a stream allocates the stream's workspace, so make one call before
  * capturing; while the stream is capturing, the allocation checks and the

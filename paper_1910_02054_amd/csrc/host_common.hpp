@@ -41,7 +41,6 @@ struct Ctx {
     zs::Result* res = nullptr;      // result record (device), read by the update kernel
     zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
     zs::Result* host_dev = nullptr; // its device-side address
-    double* dsum = nullptr;         // statistics total of the resident step (device)
     zs::AdamConst* dconst = nullptr; // fp32 constants of the resident step (device)
     hipEvent_t prof_last_end = nullptr;  // end event of the last profiled update on this stream
     uint64_t prof_tick = 0;              // steps seen while profiling (for sampling)

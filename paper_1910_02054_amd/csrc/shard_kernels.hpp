@@ -21,10 +21,10 @@
 // The other ways of running the same step swap only the one-thread kernels
 // around these: the split phase takes the global sum from the host
 // (k_set_result) or from device memory (k_finalize_sum writes a rank's local
-// sum, k_set_result_dev reads the combined one); the resident step derives the
-// scalars and the fp32 constants from a state record in device memory
-// (k_resident_prepare) and runs the loss-scale schedule there
-// (k_resident_finish).
+// sum, k_set_result_dev reads the combined one); the resident step's
+// k_resident_begin takes the finalize's place and also derives the fp32
+// constants from a state record in device memory and runs the loss-scale
+// schedule there.
 //
 // Numerics: every fp32 operation of the update is correctly rounded (IEEE
 // division and square root, no contraction), in the order Adam's bias-corrected
@@ -227,9 +227,9 @@ __global__ __launch_bounds__(BLOCK) void k_stats(const uint16_t* __restrict__ g,
 // ---------------------------------------------------------------------------
 constexpr int kFinalBlock = 256;
 
-[[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize(
-    const Partial* __restrict__ part, int nparts, Result* __restrict__ res, Result* __restrict__ res_host,
-    double loss_scale, double clip, uint32_t seq) {
+// The total of part[0, nparts) in a fixed order (every thread of the
+// kFinalBlock-thread workgroup returns it); 0 for nparts = 0.
+__device__ __forceinline__ double partials_total(const Partial* __restrict__ part, int nparts) {
     double s0 = 0.0, s1 = 0.0;
     int i = threadIdx.x;
     for (; i + kFinalBlock < nparts; i += 2 * kFinalBlock) {
@@ -238,7 +238,13 @@ constexpr int kFinalBlock = 256;
     }
     if (i < nparts)
         s0 += part[i].sumsq;
-    const double tot = block_sum<kFinalBlock>(s0 + s1);
+    return block_sum<kFinalBlock>(s0 + s1);
+}
+
+[[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize(
+    const Partial* __restrict__ part, int nparts, Result* __restrict__ res, Result* __restrict__ res_host,
+    double loss_scale, double clip, uint32_t seq) {
+    const double tot = partials_total(part, nparts);
     if (threadIdx.x == 0) {
         const Result r = make_result(tot, loss_scale, clip, seq);
         *res = r;
@@ -261,15 +267,7 @@ constexpr int kFinalBlock = 256;
 // no result record, no host copy).
 [[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize_sum(
     const Partial* __restrict__ part, int nparts, double* __restrict__ out) {
-    double s0 = 0.0, s1 = 0.0;
-    int i = threadIdx.x;
-    for (; i + kFinalBlock < nparts; i += 2 * kFinalBlock) {
-        s0 += part[i].sumsq;
-        s1 += part[i + kFinalBlock].sumsq;
-    }
-    if (i < nparts)
-        s0 += part[i].sumsq;
-    const double tot = block_sum<kFinalBlock>(s0 + s1);
+    const double tot = partials_total(part, nparts);
     if (threadIdx.x == 0)
         *out = tot;
 }
@@ -293,14 +291,21 @@ constexpr int kFinalBlock = 256;
     }
 }
 
-// Resident step, before the update: the result record from the statistics total
-// and the record's loss scale and clip, and the fp32 constants from the
-// record's hyperparameters and t (each computed in double and rounded once).
-[[maybe_unused]] static __global__ __launch_bounds__(64) void k_resident_prepare(
-    const double* __restrict__ sumsq, const zero_resident_state_t* __restrict__ st, Result* __restrict__ res,
+// Resident step, before the update, in one workgroup: the statistics total
+// (as k_finalize forms it), the result record from it and the state record's
+// loss scale and clip, the fp32 constants from the record's hyperparameters
+// and t (each computed in double and rounded once), and then the loss-scale
+// schedule on the record: after an overflow the scale halves (not below
+// min_scale) and t stays; otherwise t and the good-step count advance and the
+// scale doubles after `window` good steps.  The update kernel reads only the
+// result record and the constants, so the schedule need not wait for it.
+[[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_resident_begin(
+    const Partial* __restrict__ part, int nparts, zero_resident_state_t* __restrict__ st, Result* __restrict__ res,
     AdamConst* __restrict__ cout, uint32_t seq) {
+    const double tot = partials_total(part, nparts);
     if (threadIdx.x == 0) {
-        *res = make_result(*sumsq, st->loss_scale, st->clip, seq);
+        const Result r = make_result(tot, st->loss_scale, st->clip, seq);
+        *res = r;
         const double t = (double)st->t;
         AdamConst c;
         c.lr = (float)st->lr;
@@ -313,16 +318,9 @@ constexpr int kFinalBlock = 256;
         c.eps = (float)st->eps;
         c.wd = (float)st->weight_decay;
         *cout = c;
-    }
-}
-
-// Resident step, after the update: the loss-scale schedule on the device.
-[[maybe_unused]] static __global__ __launch_bounds__(64) void k_resident_finish(zero_resident_state_t* __restrict__ st,
-                                                                                 const Result* __restrict__ res) {
-    if (threadIdx.x == 0) {
         st->steps += 1;
-        st->skipped = res->skip;
-        if (res->skip) {
+        st->skipped = r.skip;
+        if (r.skip) {
             const double h = st->loss_scale * 0.5;
             st->loss_scale = h > st->min_scale ? h : st->min_scale;
             st->good = 0;

@@ -171,7 +171,6 @@ int get_ctx(hipStream_t stream, Ctx** out) {
         kAdamBlock, kAdamPerCU, prop, &c->adam_resident);
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
-              hipMalloc(reinterpret_cast<void**>(&c->dsum), sizeof(double)) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->dconst), sizeof(zs::AdamConst)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
@@ -179,7 +178,6 @@ int get_ctx(hipStream_t stream, Ctx** out) {
     if (!ok) {
         if (c->part) (void)hipFree(c->part);
         if (c->res) (void)hipFree(c->res);
-        if (c->dsum) (void)hipFree(c->dsum);
         if (c->dconst) (void)hipFree(c->dconst);
         if (c->host) (void)hipHostFree(c->host);
         (void)hipGetLastError();
@@ -856,16 +854,16 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
         return fail(ZERO_EHIP, "%s: could not create a profiling event", fn);
     if (prof)
         HIP_TRY(hipEventRecord(pr.start, stream));
+    // statistics, then one workgroup that totals them, fills the result record and the
+    // constants and advances the state record's loss-scale schedule (an empty shard has no
+    // partials: its total is 0), then the update
     if (n > 0) {
         zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
             <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
         HIP_TRY(hipGetLastError());
-        zs::k_finalize_sum<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->dsum);
-    } else {
-        zs::k_set_value<<<1, 64, 0, stream>>>(ctx->dsum, 0.0);
     }
-    HIP_TRY(hipGetLastError());
-    zs::k_resident_prepare<<<1, 64, 0, stream>>>(ctx->dsum, state, ctx->res, ctx->dconst, seq);
+    zs::k_resident_begin<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, n > 0 ? pl.stats_blocks : 0, state, ctx->res,
+                                                            ctx->dconst, seq);
     HIP_TRY(hipGetLastError());
     if (prof)
         HIP_TRY(hipEventRecord(pr.mid, stream));
@@ -877,8 +875,6 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
         if ((rc = prof_end(ctx, pr)))
             return rc;
     }
-    zs::k_resident_finish<<<1, 64, 0, stream>>>(state, ctx->res);
-    HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
 
