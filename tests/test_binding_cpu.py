@@ -1,6 +1,9 @@
 """The Python binding on the CPU: argument marshalling fails loudly (no host
 fallback exists), and the LAMB plan wrapper validates layer tables before
 anything reaches a device."""
+import os
+import subprocess
+import sys
 import types
 
 import numpy as np
@@ -85,3 +88,15 @@ def test_exports_match_the_loaded_library(zb):
     lib = zb.raw_library()
     for name in zb.EXPORTS:
         assert hasattr(lib, name), name
+
+
+def test_import_fails_loudly_without_the_library(tmp_path):
+    # No fallback path exists: with the library missing, importing the binding raises.
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import paper_1910_02054_amd.build as b; b.LIB = %r\n"
+            "try:\n    import paper_1910_02054_amd.binding\nexcept ImportError as e:\n    print('refused:', e)\n"
+            "else:\n    print('imported')\n" % str(tmp_path / "missing.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, stdout=subprocess.PIPE, stderr=subprocess.STDOUT,
+                       timeout=120)
+    out = r.stdout.decode(errors="replace")
+    assert "refused: libzeroshard.so is not built" in out, out
