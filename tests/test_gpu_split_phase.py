@@ -289,3 +289,45 @@ def test_async_flag_into_mapped_host_memory(env):
                             1.0)
     assert skip == 0
     say("async mapped flag", H.compare_state([b.download() for b in bufs[1:]], ref))
+
+
+@pytest.mark.parametrize("inject", [False, True])
+def test_param_groups_share_one_global_norm(env, inject):
+    # Two parameter groups of one rank with their own hyperparameters (weights with decoupled
+    # weight decay, biases and norms without, and another learning rate), each its own shard
+    # buffer; global-norm clipping over both: the local sums of the two groups are added (fixed
+    # order) and each group is applied with that global value.  Oracle: the exact sum of both
+    # groups' integer statistics, then each group's update with the shared multiplier.  An
+    # overflow in either group skips both.
+    torch, zb, dev = env
+    groups = [(3_000_017, dict(lr=1e-4, wd=0.01)), (40_961, dict(lr=2e-4, wd=0.0))]
+    scale, clip, t = 2.0 ** 16, 1.0, 3
+    state, refs, grads = [], [], []
+    for k, (n, hp) in enumerate(groups):
+        g16, theta, m, v = workloads.random_case(260 + k, n, grad_std=3e-3)
+        if inject and k == 1:
+            g16[n // 2] = 0x7E00
+        bufs = [H.Guarded(torch, n, dt, dev) for dt in (torch.float16, torch.float32, torch.float32, torch.float32,
+                                                       torch.float16)]
+        for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+            b.upload(a)
+        state.append(bufs)
+        refs.append([theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)])
+        grads.append(g16)
+    local = [zb.zero_shard_stats(b[0].view) for b in state]
+    total = local[0] + local[1]
+    flags = [zb.zero_shard_apply(*(x.view for x in b), total, hp["lr"], HP["beta1"], HP["beta2"], HP["eps"], hp["wd"],
+                                 t, scale, clip) for b, (n, hp) in zip(state, groups)]
+    torch.cuda.synchronize()
+    parts = [oracle.local_stats(g) for g in grads]
+    sc = oracle.scalars(parts[0][0] + parts[1][0], parts[0][1] | parts[1][1], scale, clip)
+    assert flags == [sc.skip, sc.skip] == ([1, 1] if inject else [0, 0])
+    if not sc.skip:
+        assert sc.coef < 1.0  # the clip is active: the shared multiplier matters
+        assert abs(total / sc.sumsq - 1) <= 1e-12
+    for b, ref, g16, (n, hp) in zip(state, refs, grads, groups):
+        if not sc.skip:
+            oracle.adam(g16, *ref, sc.mult, oracle.hyper(hp["lr"], HP["beta1"], HP["beta2"], HP["eps"], hp["wd"], t))
+        d = H.compare_state([x.download() for x in b[1:]], ref)
+        say("group n", n, "skip", sc.skip, d)
+        assert all(x.guards_intact() for x in b)
