@@ -120,6 +120,25 @@ def _addr(x, dtypes=None, what="array"):
     return x.data_ptr()
 
 
+def _shard_len(n, *arrays):
+    """The element count of a shard call.  With n None: the common length of the tensors
+    (all arguments must be tensors).  An explicit n may not exceed any tensor's length;
+    for raw integer addresses the caller vouches for the size."""
+    ts = [a for a in arrays if a is not None and not isinstance(a, int)]
+    if n is None:
+        if not ts or len(ts) != len(arrays):
+            raise ValueError("n is required unless every array is a tensor")
+        n = ts[0].numel()
+        if any(t.numel() != n for t in ts):
+            raise ValueError("shard tensors differ in length")
+        return n
+    n = int(n)
+    for t in ts:
+        if t.numel() < n:
+            raise ValueError("n = %d exceeds a tensor of %d elements" % (n, t.numel()))
+    return n
+
+
 def _stream(stream):
     if stream is None:
         import torch
@@ -144,11 +163,7 @@ def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, e
     import torch
     h16 = (torch.float16, torch.int16)
     f32 = (torch.float32,)
-    if n is None:
-        n = grad16.numel()
-        for t in (master32, m32, v32, param16_out):
-            if t.numel() != n:
-                raise ValueError("shard tensors differ in length")
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
     return _check(_lib.zero_shard_step(
         _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(lr), float(beta1),
@@ -159,8 +174,7 @@ def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, e
 def zero_shard_stats(grad16, n=None, stream=None) -> float:
     """Local sum of squares of a shard's loss-scaled fp16 gradients (fp64; inf/NaN on overflow)."""
     import torch
-    if n is None:
-        n = grad16.numel()
+    n = _shard_len(n, grad16)
     out = ctypes.c_double()
     _check(_lib.zero_shard_stats(_addr(grad16, (torch.float16, torch.int16), "grad16"), int(n), ctypes.byref(out),
                                  _stream(stream)))
@@ -173,11 +187,7 @@ def zero_shard_apply(grad16, master32, m32, v32, param16_out, global_sumsq, lr, 
     import torch
     h16 = (torch.float16, torch.int16)
     f32 = (torch.float32,)
-    if n is None:
-        n = grad16.numel()
-        for t in (master32, m32, v32, param16_out):
-            if t.numel() != n:
-                raise ValueError("shard tensors differ in length")
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
     return _check(_lib.zero_shard_apply(
         _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(global_sumsq), float(lr),
@@ -189,8 +199,7 @@ def zero_shard_stats_async(grad16, local_sumsq, n=None, stream=None):
     """Enqueue the shard's sum of squares into local_sumsq (a float64 device tensor
     of one element, or a device address); returns without waiting."""
     import torch
-    if n is None:
-        n = grad16.numel()
+    n = _shard_len(n, grad16)
     _check(_lib.zero_shard_stats_async(_addr(grad16, (torch.float16, torch.int16), "grad16"), int(n),
                                        _addr(local_sumsq, (torch.float64,), "local_sumsq"), _stream(stream)))
 
@@ -203,11 +212,7 @@ def zero_shard_apply_async(grad16, master32, m32, v32, param16_out, global_sumsq
     import torch
     h16 = (torch.float16, torch.int16)
     f32 = (torch.float32,)
-    if n is None:
-        n = grad16.numel()
-        for t in (master32, m32, v32, param16_out):
-            if t.numel() != n:
-                raise ValueError("shard tensors differ in length")
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
     _check(_lib.zero_shard_apply_async(
         _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n),
@@ -237,11 +242,7 @@ def zero_shard_step_resident(grad16, master32, m32, v32, param16_out, state, n=N
     import torch
     h16 = (torch.float16, torch.int16)
     f32 = (torch.float32,)
-    if n is None:
-        n = grad16.numel()
-        for t in (master32, m32, v32, param16_out):
-            if t.numel() != n:
-                raise ValueError("shard tensors differ in length")
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
     if not isinstance(state, int) and state.numel() * state.element_size() < ctypes.sizeof(ResidentState):
         raise ValueError("state must hold a zero_resident_state_t (%d bytes)" % ctypes.sizeof(ResidentState))
     _check(_lib.zero_shard_step_resident(
@@ -305,6 +306,9 @@ def zero_profile_read() -> Profile:
 def zero_probe_copy(src, dst, nbytes=None, stream=None):
     if nbytes is None:
         nbytes = src.numel() * src.element_size()
+    for t in (src, dst):
+        if not isinstance(t, int) and t.numel() * t.element_size() < nbytes:
+            raise ValueError("nbytes = %d exceeds a buffer of %d bytes" % (nbytes, t.numel() * t.element_size()))
     _check(_lib.zero_probe_copy(_addr(src), _addr(dst), int(nbytes), _stream(stream)))
 
 

@@ -100,3 +100,18 @@ def test_import_fails_loudly_without_the_library(tmp_path):
                        timeout=120)
     out = r.stdout.decode(errors="replace")
     assert "refused: libzeroshard.so is not built" in out, out
+
+
+def test_explicit_n_may_not_exceed_the_tensors(zb):
+    # checked before any address is taken: a too-large n never reaches the library
+    g, th, m, v, p = _cpu_shard(8)
+    with pytest.raises(ValueError, match="exceeds a tensor of 8 elements"):
+        zb.zero_shard_step(g, th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0, n=9)
+    with pytest.raises(ValueError, match="exceeds"):
+        zb.zero_shard_stats(g, n=100)
+    with pytest.raises(ValueError, match="exceeds"):
+        zb.zero_shard_apply(g, th, m, v, p, 1.0, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0, n=9)
+    with pytest.raises(ValueError, match="n is required"):
+        zb.zero_shard_step(0x1000, th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
+    with pytest.raises(ValueError, match="exceeds a buffer"):
+        zb.zero_probe_copy(torch.zeros(4), torch.zeros(8), 32)
