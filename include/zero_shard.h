@@ -208,13 +208,11 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
  * NULL pointers, alignment, that each array [p, p + n*size) lies inside one
  * GPU-accessible allocation (hipMemGetAddressRange), then overlap.
  * zero_shard_step, zero_shard_apply and zero_shard_stats make the same
- * allocation check, so an n that overruns its allocation or a pageable host
- * pointer is rejected with ZERO_EINVAL rather than faulting the GPU.  Limits:
- * the allocation is what the HIP runtime handed out, so a caching allocator's
- * segment (larger than the tensor carved from it) bounds the check; and step
- * and apply remember the last (arrays, n) that passed on each stream and skip
- * the lookup while they repeat, so a buffer freed and re-allocated smaller at
- * the same address is caught only by calling this function.
+ * allocation check on every call (a lookup costs well under a microsecond), so
+ * an n that overruns its allocation or a pageable host pointer is rejected with
+ * ZERO_EINVAL rather than faulting the GPU.  Limit: the allocation is what the
+ * HIP runtime handed out, so a caching allocator's segment (larger than the
+ * tensor carved from it) bounds the check.
  * Returns 0 or ZERO_EINVAL. */
 int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
                         const uint16_t* param16_out, int64_t n);

@@ -48,7 +48,6 @@ struct Ctx {
     int ncu = 0;
     size_t stats_lds = 0, adam_lds = 0;   // occupancy reservations (dynamic LDS per workgroup)
     int stats_resident = 0, adam_resident = 0;
-    uintptr_t checked[6] = {0, 0, 0, 0, 0, 0};  // last (arrays, n) whose ranges were verified
 };
 
 // The context of (current device, stream), created on first use; rejects a

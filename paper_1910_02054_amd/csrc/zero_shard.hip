@@ -354,21 +354,6 @@ int check_shard_ranges(const char* fn, const uint16_t* grad16, const float* mast
     return check_ranges(fn, ptrs, bytes, 5);
 }
 
-// The range check once per distinct (arrays, n) on a stream: a training loop
-// that reuses its buffers pays for it once.
-int check_shard_ranges_cached(Ctx* ctx, const char* fn, const uint16_t* grad16, const float* master32,
-                              const float* m32, const float* v32, const uint16_t* param16_out, int64_t n) {
-    const uintptr_t key[6] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
-                              reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
-                              reinterpret_cast<uintptr_t>(param16_out), (uintptr_t)n};
-    if (std::memcmp(key, ctx->checked, sizeof key) == 0)
-        return ZERO_OK;
-    const int rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n);
-    if (rc == ZERO_OK)
-        std::memcpy(ctx->checked, key, sizeof key);
-    return rc;
-}
-
 // fp32 constants, each computed in double and rounded once (the bias
 // corrections 1 - beta^t use the C library's pow).
 zs::AdamConst adam_const(double lr, double beta1, double beta2, double eps, double wd, int64_t step) {
@@ -591,7 +576,7 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     if ((rc = get_ctx(stream, &ctx)))
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
-    if ((rc = check_shard_ranges_cached(ctx, "zero_shard_step", grad16, master32, m32, v32, param16_out, n)))
+    if ((rc = check_shard_ranges("zero_shard_step", grad16, master32, m32, v32, param16_out, n)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
@@ -681,7 +666,7 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     if ((rc = get_ctx(stream, &ctx)))
         return rc;
     std::lock_guard<std::mutex> lk(ctx->mu);
-    if ((rc = check_shard_ranges_cached(ctx, "zero_shard_apply", grad16, master32, m32, v32, param16_out, n)))
+    if ((rc = check_shard_ranges("zero_shard_apply", grad16, master32, m32, v32, param16_out, n)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
     const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
@@ -781,7 +766,7 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
         if ((rc = check_ranges(fn, ptrs, bytes, skipped ? 2 : 1)))
             return rc;
     }
-    if (n > 0 && (rc = check_shard_ranges_cached(ctx, fn, grad16, master32, m32, v32, param16_out, n)))
+    if (n > 0 && (rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
         return rc;
     const uint32_t seq = next_seq(ctx);
     if (n == 0) {
@@ -843,7 +828,7 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
         const size_t bytes = sizeof *state;
         if ((rc = check_ranges(fn, &ptr, &bytes, 1)))
             return rc;
-        if (n > 0 && (rc = check_shard_ranges_cached(ctx, fn, grad16, master32, m32, v32, param16_out, n)))
+        if (n > 0 && (rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
             return rc;
     }
     const uint32_t seq = next_seq(ctx);

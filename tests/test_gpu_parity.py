@@ -395,3 +395,48 @@ def test_validate_catches_overruns_and_host_memory(env):
     with pytest.raises(zb.ZeroError) as e:
         zb.zero_shard_validate(*(h.ctypes.data for h in host), n)
     assert e.value.code == zb.ZERO_EINVAL
+
+
+def test_reallocated_smaller_buffer_is_rejected(env):
+    # The allocation check runs on every call: after a step on five 8M-element buffers, the
+    # gradient buffer is freed and a 1 MiB one allocated (often at the same address); a step
+    # with the old n must be refused before any launch.  Raw hipMalloc/hipFree, outside torch's
+    # caching allocator, so the allocations are exactly the requested sizes.
+    import ctypes
+    torch, zb, dev = env
+    # the HIP runtime already in the process (torch and the library share it): never a second copy
+    hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD)
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    hip.hipFree.argtypes = [ctypes.c_void_p]
+    hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    n = 8 << 20
+    sizes = (2 * n, 4 * n, 4 * n, 4 * n, 2 * n)
+    ptrs = []
+    for sz in sizes:
+        p = ctypes.c_void_p()
+        assert hip.hipMalloc(ctypes.byref(p), sz) == 0
+        ptrs.append(p.value)
+    try:
+        zero16 = torch.zeros(n, dtype=torch.float16, device=dev)
+        zero32 = torch.zeros(n, dtype=torch.float32, device=dev)
+        for i, p in enumerate(ptrs):  # defined contents: zero gradients and state
+            src = zero16 if sizes[i] == 2 * n else zero32
+            assert hip.hipMemcpy(p, src.data_ptr(), sizes[i], 3) == 0  # device to device
+        torch.cuda.synchronize()
+        assert zb.zero_shard_step(*ptrs, 1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 0.0, n=n) == 0
+        torch.cuda.synchronize()
+        old = ptrs[0]
+        assert hip.hipFree(ptrs[0]) == 0
+        p = ctypes.c_void_p()
+        assert hip.hipMalloc(ctypes.byref(p), 1 << 20) == 0
+        ptrs[0] = p.value
+        say("re-allocated gradient buffer", "at the same address" if p.value == old else "elsewhere")
+        with pytest.raises(zb.ZeroError) as e:
+            zb.zero_shard_step(*ptrs, 1e-4, 0.9, 0.999, 1e-8, 0.0, 2, 1.0, 0.0, n=n)
+        assert e.value.code == zb.ZERO_EINVAL and "overruns" in str(e.value)
+        with pytest.raises(zb.ZeroError):
+            zb.zero_shard_apply(*ptrs, 0.0, 1e-4, 0.9, 0.999, 1e-8, 0.0, 2, 1.0, 0.0, n=n)
+    finally:
+        torch.cuda.synchronize()
+        for p in ptrs:
+            hip.hipFree(p)
