@@ -232,7 +232,9 @@ def resident_state(device, lr, beta1, beta2, eps, weight_decay, clip, loss_scale
 
 
 def read_resident_state(state_tensor) -> ResidentState:
-    """The record's current contents (copies to the host: synchronises with its stream)."""
+    """The record's contents, copied to the host.  The copy is ordered after the work of
+    torch's current stream only: after resident steps on another stream, synchronise that
+    stream first."""
     return ResidentState.from_buffer_copy(bytes(state_tensor.cpu().numpy().tobytes()))
 
 
