@@ -440,3 +440,38 @@ def test_reallocated_smaller_buffer_is_rejected(env):
         torch.cuda.synchronize()
         for p in ptrs:
             hip.hipFree(p)
+
+
+def test_workspace_does_not_grow_with_the_shard(env):
+    # Sec. 6.2's constant-size buffers: the library's own device memory for a step is a
+    # fixed-size workspace per (device, stream), whatever n is.  Device free memory is read
+    # through the HIP runtime around single calls on fresh streams (first a 1M-element shard,
+    # then a 200M-element one); no Psi-sized temporary may appear.
+    import ctypes
+    torch, zb, dev = env
+    hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD)
+    hip.hipMemGetInfo.argtypes = [ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_size_t)]
+
+    def free_bytes():
+        torch.cuda.synchronize()
+        f, t = ctypes.c_size_t(), ctypes.c_size_t()
+        assert hip.hipMemGetInfo(ctypes.byref(f), ctypes.byref(t)) == 0
+        return f.value
+
+    deltas = {}
+    for n in (1 << 20, 200_000_000):
+        bufs = _alloc(torch, dev, n)
+        for b, a in zip(bufs, (np.zeros(n, np.uint16), np.zeros(n, np.float32), np.zeros(n, np.float32),
+                               np.zeros(n, np.float32), np.zeros(n, np.uint16))):
+            b.upload(a)
+        s = torch.cuda.Stream()
+        before = free_bytes()
+        flag = zb.zero_shard_step(*(b.view for b in bufs), 1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 0.0, stream=s)
+        s.synchronize()
+        deltas[n] = before - free_bytes()
+        say("workspace on a fresh stream, n", n, "device bytes", deltas[n])
+        assert flag == 0
+        del bufs
+        torch.cuda.empty_cache()
+    assert deltas[200_000_000] <= deltas[1 << 20] + (2 << 20)   # nothing proportional to n
+    assert deltas[200_000_000] < (16 << 20)                      # 800 MB would be 4 B/element
