@@ -146,6 +146,37 @@ def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
                       "update), single thread, %.1f s" % (done, n, t_used), **_host_cpu()}
 
 
+def cpu_baseline_parallel(w, n, theta, m, v, g16, scale, budget_s):
+    """The oracle's whole-shard step, unchanged, spread over the host cores this process may
+    use: the exact integer statistics of 4M-element chunks in parallel threads (the oracle is
+    C called through ctypes, which releases the interpreter lock), their sum and the shared
+    scalars, then the element-wise update of every chunk in parallel with the shared
+    multiplier; whole passes over a copy of the shard state until about budget_s seconds."""
+    from concurrent.futures import ThreadPoolExecutor
+    import numpy as np
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    spans = [(a, min(n, a + (1 << 22))) for a in range(0, n, 1 << 22)]
+    th, mm, vv = theta.copy(), m.copy(), v.copy()
+    p16 = np.empty(n, np.uint16)
+    hp = oracle.hyper(w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, 1)
+    done, t_used, passes = 0, 0.0, 0
+    with ThreadPoolExecutor(max_workers=cores) as ex:
+        while t_used < budget_s:
+            t0 = time.perf_counter()
+            parts = list(ex.map(lambda s: oracle.local_stats(g16[s[0]:s[1]]), spans))
+            sc = oracle.scalars(sum(q[0] for q in parts), max(q[1] for q in parts), scale, w.clip)
+            if not sc.skip:
+                list(ex.map(lambda s: oracle.adam(g16[s[0]:s[1]], th[s[0]:s[1]], mm[s[0]:s[1]], vv[s[0]:s[1]],
+                                                  p16[s[0]:s[1]], sc.mult, hp), spans))
+            t_used += time.perf_counter() - t0
+            done += n
+            passes += 1
+    return {"value": done / t_used, "unit": "params/s", "cores": cores, "kind": "oracle",
+            "sample": "%d whole-shard oracle steps of %d elements (exact statistics of all chunks, then the "
+                      "update), %d threads, %.1f s" % (passes, n, cores, t_used), **_host_cpu()}
+
+
 def lamb_cpu_baseline(w, seg, theta, m, v, g16, scale, budget_s):
     """The oracle's LAMB step, as it stands, single-threaded on whole layers of the
     shard in order (a layer's trust ratio needs all of it), until about budget_s
@@ -178,6 +209,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle CPU time")
+    ap.add_argument("--cpu-parallel-budget", type=float, default=5.0,
+                    help="adam only: seconds of the oracle's whole-shard step on all usable host cores "
+                         "(reported as cpu_baseline_parallel; 0 = off)")
     ap.add_argument("--step-samples", type=int, default=50,
                     help="after the timed region, time this many further steps one by one with HIP events "
                          "(median, p10, p90 of single steps; 0 = off)")
@@ -448,6 +482,10 @@ def main():
             out["cpu_baseline"] = lamb_cpu_baseline(w, seg, theta, m, v, g16, w.loss_scale, args.cpu_budget)
         else:
             out["cpu_baseline"] = cpu_baseline(w, n, theta, m, v, g16, w.loss_scale, args.cpu_budget)
+            if args.cpu_parallel_budget > 0:
+                print("[bench] parallel cpu baseline (oracle)", file=sys.stderr, flush=True)
+                out["cpu_baseline_parallel"] = cpu_baseline_parallel(w, n, theta, m, v, g16, w.loss_scale,
+                                                                     args.cpu_parallel_budget)
     if plan is not None:
         plan.close()
     print(json.dumps(out), flush=True)

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 def _run(*extra):
     cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny", "--steps", "50", "--warmup", "5",
-           "--step-samples", "10", "--probe-copy-mib", "64", "--cpu-budget", "0.5", *extra]
+           "--step-samples", "10", "--probe-copy-mib", "64", "--cpu-budget", "0.5", "--cpu-parallel-budget", "0.5",
+           *extra]
     print("[gpu-bench-contract]", " ".join(cmd[1:]), flush=True)
     r = subprocess.run(cmd, cwd=ROOT, stdout=subprocess.PIPE, stderr=subprocess.PIPE, timeout=110)
     assert r.returncode == 0, r.stderr.decode(errors="replace")[-2000:]
@@ -44,7 +45,10 @@ def _check(d, kernel):
 
 
 def test_adam_line():
-    _check(_run(), "k_adam_vec")
+    d = _run()
+    _check(d, "k_adam_vec")
+    cp = d["cpu_baseline_parallel"]
+    assert cp["kind"] == "oracle" and cp["cores"] >= 1 and cp["value"] > 0 and cp["unit"] == "params/s"
 
 
 def test_lamb_line():
