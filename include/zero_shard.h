@@ -102,7 +102,10 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
  *
  * All five arrays must be distinct, non-overlapping ranges; base pointers of
  * any element alignment are accepted (when all five share one misalignment
- * the vectorised path runs after a few scalar head elements).  The call
+ * the vectorised path runs after a few scalar head elements).  Placement
+ * affects speed, not results: separate allocations, or arrays packed into one
+ * buffer each on its own 2 MiB boundary, run fastest; arrays offset from one
+ * another by a few hundred bytes run about 5 % slower.  The call
  * blocks until the skip decision is known (the statistics kernels publish it
  * in host-mapped memory, which the calling thread polls); the update kernel
  * may still be running on `stream` when it returns.  Returns 0 applied,
