@@ -148,7 +148,7 @@ def cpu_baseline(w, n, theta, m, v, g16, scale, budget_s):
 
 def cpu_baseline_parallel(w, n, theta, m, v, g16, scale, budget_s):
     """The oracle's whole-shard step, unchanged, spread over the host cores this process may
-    use: the exact integer statistics of 4M-element chunks in parallel threads (the oracle is
+    use: the exact integer statistics of chunks (at most 4M elements) in parallel threads (the oracle is
     C called through ctypes, which releases the interpreter lock), their sum and the shared
     scalars, then the element-wise update of every chunk in parallel with the shared
     multiplier; whole passes over a copy of the shard state until about budget_s seconds."""
@@ -156,7 +156,9 @@ def cpu_baseline_parallel(w, n, theta, m, v, g16, scale, budget_s):
     import numpy as np
     import oracle
     cores = len(os.sched_getaffinity(0))
-    spans = [(a, min(n, a + (1 << 22))) for a in range(0, n, 1 << 22)]
+    chunk = max(1 << 16, min(1 << 22, -(-n // (4 * cores))))  # at least four chunks per thread when n allows
+    spans = [(a, min(n, a + chunk)) for a in range(0, n, chunk)]
+    cores = min(cores, len(spans))                              # the threads that can have work
     th, mm, vv = theta.copy(), m.copy(), v.copy()
     p16 = np.empty(n, np.uint16)
     hp = oracle.hyper(w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, 1)
