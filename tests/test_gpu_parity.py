@@ -473,5 +473,5 @@ def test_workspace_does_not_grow_with_the_shard(env):
         assert flag == 0
         del bufs
         torch.cuda.empty_cache()
-    assert deltas[200_000_000] <= deltas[1 << 20] + (2 << 20)   # nothing proportional to n
-    assert deltas[200_000_000] < (16 << 20)                      # 800 MB would be 4 B/element
+    # nothing proportional to n: one byte per element would already be 200 MB at the larger size
+    assert all(d < (16 << 20) for d in deltas.values()), deltas
