@@ -139,10 +139,21 @@ def _shard_len(n, *arrays):
     return n
 
 
+_raw_stream = None
+
+
 def _stream(stream):
+    """The hipStream_t of `stream` (a torch stream, a raw handle, or None for torch's current
+    stream on the current device).  The current stream's handle is read without building a
+    torch Stream object (which costs a few microseconds per call)."""
+    global _raw_stream
     if stream is None:
         import torch
-        return torch.cuda.current_stream().cuda_stream
+        if _raw_stream is None:
+            getter = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+            _raw_stream = (lambda: getter(torch.cuda.current_device())) if getter is not None else \
+                (lambda: torch.cuda.current_stream().cuda_stream)
+        return _raw_stream()
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
