@@ -1,6 +1,5 @@
-"""Helpers shared by the GPU parity tests, the smoke check and the benchmark's
-CPU-baseline leg: guarded device buffers, a thread-parallel driver of the CPU
-oracle, and the parity comparison.
+"""Helpers shared by the GPU parity tests and the smoke check: guarded device
+buffers, a thread-parallel driver of the CPU oracle, and the parity comparison.
 
 The oracle is run chunk by chunk in threads (ctypes releases the GIL): exact
 per-chunk sums of squares are added as integers and the element-wise update is
