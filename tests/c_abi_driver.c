@@ -13,7 +13,9 @@
  * shifted by different counts (scalar path); per case three fused steps, the
  * second with an inf gradient (skipped, nothing written), then one split-phase
  * step (zero_shard_stats, then zero_shard_apply with that sum as the global
- * one), each compared byte for byte with the oracle.
+ * one), each compared byte for byte with the oracle; then LAMB steps through a
+ * layer-table plan (tiny layers, layers across tile boundaries) at the same
+ * three alignments.
  */
 #include <hip/hip_runtime_api.h>
 
@@ -24,10 +26,14 @@
 
 #include "zero_shard.h"
 
-/* The oracle's shard step (oracle/zero_oracle.c); its last argument may be NULL. */
+/* The oracle's shard steps (oracle/zero_oracle.c); the scalar and per-layer outputs may be NULL. */
 int zo_shard_step(const uint16_t* g16, float* theta, float* m, float* v, uint16_t* p16, int64_t n, double lr,
                   double beta1, double beta2, double eps, double wd, int64_t t, double loss_scale, double clip,
                   void* scalars_out);
+int zo_lamb_step(const uint16_t* g16, float* theta, float* m, float* v, uint16_t* p16, int64_t n,
+                 const int64_t* seg_off, int32_t n_seg, double lr, double beta1, double beta2, double eps,
+                 double wd, int64_t t, double loss_scale, double clip, double phi_lo, double phi_hi,
+                 void* scalars_out, double* seg_out);
 
 #define LR 1e-4
 #define B1 0.9
@@ -193,6 +199,78 @@ static int run_case(int64_t n, const int shift[5], hipStream_t stream) {
     return ok;
 }
 
+/* LAMB (ZeRO Sec. 2.3 lists it among the optimizers whose state partitioning
+ * makes affordable): one step over a layer table with a few tiny layers and
+ * layers that do not line up with the kernels' tiles, through a plan. */
+static int run_lamb_case(int64_t n, const int shift[5], hipStream_t stream) {
+    shard_t s;
+    char what[128];
+    int64_t off[16];
+    int32_t n_seg = 0;
+    const int64_t cuts[] = {1, 2, 5, 517, 4096, 4099, 70001};
+    off[n_seg] = 0;
+    for (size_t k = 0; k < sizeof cuts / sizeof cuts[0]; ++k)
+        if (cuts[k] > off[n_seg] && cuts[k] < n)
+            off[++n_seg] = cuts[k];
+    off[++n_seg] = n;
+    for (int i = 0; i < 5; ++i) {
+        HIPCHECK(hipMalloc(&s.d[i], kSize[i] * (size_t)(n + PAD)));
+        s.view[i] = (char*)s.d[i] + kSize[i] * (size_t)shift[i];
+    }
+    s.g = malloc(2 * (size_t)n);
+    s.p = malloc(2 * (size_t)n);
+    s.th = malloc(4 * (size_t)n);
+    s.m = malloc(4 * (size_t)n);
+    s.v = malloc(4 * (size_t)n);
+    for (int64_t k = 0; k < n; ++k) {
+        s.g[k] = rnd_f16();
+        s.th[k] = rnd_f32(110, 126, 0);
+        s.m[k] = rnd_f32(100, 115, 0);
+        s.v[k] = rnd_f32(90, 110, 1);
+        s.p[k] = SENTINEL;
+    }
+    for (int i = 0; i < 5; ++i)
+        upload(&s, i, i == 0 ? (const void*)s.g : i == 1 ? (const void*)s.th : i == 2 ? (const void*)s.m
+                                                  : i == 3 ? (const void*)s.v : (const void*)s.p, n);
+    zero_lamb_plan_t* plan = NULL;
+    int ok = 1;
+    int rc = zero_lamb_plan_create(off, n_seg, n, &plan);
+    snprintf(what, sizeof what, "lamb n=%lld layers=%d shifts=%d%d%d%d%d", (long long)n, n_seg, shift[0], shift[1],
+             shift[2], shift[3], shift[4]);
+    if (rc != ZERO_OK) {
+        printf("FAIL: %s: plan: %s\n", what, zero_last_error());
+        ok = 0;
+    } else {
+        rc = zero_lamb_step(plan, (const uint16_t*)s.view[0], (float*)s.view[1], (float*)s.view[2],
+                            (float*)s.view[3], (uint16_t*)s.view[4], LR, B1, B2, 1e-6, WD, 3, SCALE, CLIP, 0.0,
+                            10.0, stream);
+        HIPCHECK(hipStreamSynchronize(stream));
+        const int want = zo_lamb_step(s.g, s.th, s.m, s.v, s.p, n, off, n_seg, LR, B1, B2, 1e-6, WD, 3, SCALE,
+                                      CLIP, 0.0, 10.0, NULL, NULL);
+        if (rc != want) {
+            printf("FAIL: %s: zero_lamb_step returned %d (%s), the oracle %d\n", what, rc, zero_last_error(), want);
+            ok = 0;
+        } else {
+            ok = check_all(&s, n, what);
+        }
+        if (zero_lamb_plan_destroy(plan) != ZERO_OK) {
+            printf("FAIL: %s: plan destroy: %s\n", what, zero_last_error());
+            ok = 0;
+        }
+    }
+    for (int i = 0; i < 5; ++i)
+        HIPCHECK(hipFree(s.d[i]));
+    free(s.g);
+    free(s.p);
+    free(s.th);
+    free(s.m);
+    free(s.v);
+    if (ok)
+        printf("ok: %s\n", what);
+    fflush(stdout);
+    return ok;
+}
+
 int main(void) {
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
@@ -214,6 +292,11 @@ int main(void) {
     }
     /* the null stream too */
     ok = ok && run_case(262147, equal, NULL);
+    /* LAMB through its plan */
+    const int64_t lamb_sizes[] = {3, 600, 100003};
+    for (size_t k = 0; k < sizeof lamb_sizes / sizeof lamb_sizes[0] && ok; ++k)
+        ok = run_lamb_case(lamb_sizes[k], aligned, stream) && run_lamb_case(lamb_sizes[k], equal, stream) &&
+             run_lamb_case(lamb_sizes[k], mixed, stream);
     HIPCHECK(hipStreamDestroy(stream));
     printf(ok ? "c-abi driver: all cases match the oracle\n" : "c-abi driver: FAILED\n");
     return ok ? 0 : 1;
