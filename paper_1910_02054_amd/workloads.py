@@ -176,7 +176,8 @@ def random_case(seed: int, n: int, grad_std: float = 1e-3, loss_scale: float = 2
         m = np.zeros(n, np.float32)
         v = np.zeros(n, np.float32)
     z = r.standard_normal(n, dtype=np.float32) * np.float32(grad_std * loss_scale)
-    g16 = z.astype(np.float16).view(np.uint16).copy()
+    with np.errstate(over="ignore"):  # a scale too large for fp16 gives inf, as in training
+        g16 = z.astype(np.float16).view(np.uint16).copy()
     return g16, master, m, v
 
 

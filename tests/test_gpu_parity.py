@@ -475,3 +475,35 @@ def test_workspace_does_not_grow_with_the_shard(env):
         torch.cuda.empty_cache()
     # nothing proportional to n: one byte per element would already be 200 MB at the larger size
     assert all(d < (16 << 20) for d in deltas.values()), deltas
+
+
+def test_loss_scale_too_large_overflows_then_recovers(env):
+    # Dynamic loss scaling's own failure mode: at 2^24 the fp16 cast of the scaled gradients
+    # overflows (inf in the generated gradient itself, not an injected one), so the step skips
+    # and the scaler halves the scale, and keeps halving while the gradients still overflow;
+    # the first scale at which they fit applies the step, which must match the oracle.
+    torch, zb, dev = env
+    n = 200_003
+    _, theta, m, v = workloads.random_case(77, n)
+    bufs = _alloc(torch, dev, n)
+    for b, a in zip(bufs[1:], (theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)]
+    scaler = zb.Scaler(2.0 ** 24)
+    flags = []
+    for _ in range(12):
+        scale = scaler.scale
+        g16 = workloads.random_case(78, n, grad_std=0.05, loss_scale=scale)[0]   # same gradient, rescaled
+        bufs[0].upload(g16)
+        flag = zb.zero_shard_step(*(b.view for b in bufs), 1e-4, 0.9, 0.999, 1e-8, 0.0, scaler.t_next, scale, 1.0)
+        torch.cuda.synchronize()
+        skip, _ = H.oracle_step(g16, *ref, 1e-4, 0.9, 0.999, 1e-8, 0.0, scaler.t_next, scale, 1.0)
+        assert flag == skip
+        flags.append(flag)
+        scaler.update(flag)
+        H.compare_state([b.download() for b in bufs[1:]], ref)
+        if not flag:
+            break
+    say("scale sequence flags", flags, "applied at scale", scale)
+    assert flags[0] == 1 and flags[-1] == 0 and scaler.t_next == 2
+    assert all(b.guards_intact() for b in bufs)
