@@ -13,10 +13,12 @@
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
+#include <chrono>
 #include <map>
 #include <memory>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -423,8 +425,14 @@ int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32,
 int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out) {
     uint64_t polls = 0;
     while (__atomic_load_n(&ctx->host->seq, __ATOMIC_ACQUIRE) != seq) {
-        __builtin_ia32_pause();
-        if ((++polls & 0xFFF) == 0) {
+        // spin for the usual wait (the statistics of one shard: microseconds); once the stream
+        // has been busy for a few milliseconds (other work queued ahead), sleep between checks
+        // instead of holding a core
+        if (polls < ((uint64_t)1 << 18))
+            __builtin_ia32_pause();
+        else
+            std::this_thread::sleep_for(std::chrono::microseconds(50));
+        if ((++polls & 0xFFF) == 0 || polls > ((uint64_t)1 << 18)) {
             const hipError_t e = hipStreamQuery(stream);
             if (e == hipSuccess) {  // everything queued has finished
                 if (__atomic_load_n(&ctx->host->seq, __ATOMIC_ACQUIRE) == seq)

@@ -507,3 +507,30 @@ def test_loss_scale_too_large_overflows_then_recovers(env):
     say("scale sequence flags", flags, "applied at scale", scale)
     assert flags[0] == 1 and flags[-1] == 0 and scaler.t_next == 2
     assert all(b.guards_intact() for b in bufs)
+
+
+def test_step_waits_behind_queued_work(env):
+    # Work queued ahead of the step on its stream (a bounded spin kernel of about 50 ms) makes the
+    # host wait long enough to leave the spinning phase and poll with sleeps; the step's result
+    # is unchanged.
+    import time
+    torch, zb, dev = env
+    n = 100_003
+    g16, theta, m, v = workloads.random_case(61, n)
+    bufs = _alloc(torch, dev, n)
+    for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)]
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        torch.cuda._sleep(120_000_000)   # clock cycles
+        t0 = time.perf_counter()
+        flag = zb.zero_shard_step(*(b.view for b in bufs), 1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 2.0 ** 16, 1.0)
+        waited = time.perf_counter() - t0
+    s.synchronize()
+    say("host wait behind queued work: %.1f ms" % (waited * 1e3))
+    skip, _ = H.oracle_step(g16, *ref, 1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 2.0 ** 16, 1.0)
+    assert flag == skip == 0
+    H.compare_state([b.download() for b in bufs[1:]], ref)
+    assert all(b.guards_intact() for b in bufs)
