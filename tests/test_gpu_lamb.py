@@ -187,7 +187,7 @@ def test_lamb_deterministic(env):
         assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
 
 
-@pytest.mark.parametrize("psi,nd", [(4_194_304, 4), (1_000_003, 7)])
+@pytest.mark.parametrize("psi,nd", [(4_194_304, 4), (1_000_003, 7), (333_331, 13), (2_000_001, 3)])
 def test_lamb_split_phase_layers_across_shards(env, psi, nd):
     # N_d ranks emulated on one GPU; the model's layers straddle shard boundaries, so each
     # rank's boundary layers need the neighbours' partial sums (exchanged here in rank order)
