@@ -229,6 +229,8 @@ def main():
     ap.add_argument("--resident", choices=("eager", "graph"), default=None,
                     help="adam only: the resident step (state record and loss scaler on the device, no host "
                          "wait), called eagerly or replayed from a captured HIP graph")
+    ap.add_argument("--no-lamb-probes", dest="lamb_probes", action="store_false",
+                    help="lamb only: skip the byte-mix probes of the two passes (run after the timed steps)")
     ap.add_argument("--async-seam", action="store_true",
                     help="with --split-phase: the asynchronous calls (sums in device memory, no host wait; the "
                          "skip flags are checked after the timed region)")
@@ -478,6 +480,27 @@ def main():
     if probe:
         probe["update_frac_of_copy"] = upd_gbps / probe["gbps"]
         out["copy_probe"] = probe
+    if lamb and args.lamb_probes:
+        # the byte mixes of the two LAMB passes at their launch shape with trivial arithmetic
+        # (after every timed step: the probes overwrite the state), timed with events on the stream
+        print("[bench] lamb byte-mix probes", file=sys.stderr, flush=True)
+        probes = {}
+        for pass_, name, bpp, got in ((0, "moments", LAMB_MOMENTS_BYTES_PER_PARAM, upd_gbps),
+                                      (1, "apply", LAMB_APPLY_BYTES_PER_PARAM, apply_gbps)):
+            arrs = (d_gs[0], d_theta, d_m, d_v, None) if pass_ == 0 else (None, d_theta, d_m, d_v, d_p)
+            for _ in range(3):
+                zb.zero_probe_lamb_pass(pass_, *arrs, n=n, stream=stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = 20
+            e0.record(stream)
+            for _ in range(reps):
+                zb.zero_probe_lamb_pass(pass_, *arrs, n=n, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            pms = e0.elapsed_time(e1) / reps
+            pg = bpp * n / (pms * 1e-3) / 1e9
+            probes[name] = {"probe_ms": pms, "probe_gbps": pg, "pass_gbps": got, "pass_frac_of_probe": got / pg}
+        out["lamb_probes"] = probes
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         if lamb:

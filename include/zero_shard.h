@@ -18,15 +18,19 @@
  *   - Array arguments are DEVICE pointers owned by the caller.  The library
  *     never allocates, frees or retains them and touches exactly [0, n).
  *   - The library owns a small per-(device, stream) workspace (per-workgroup
- *     partial sums, one result record, one pinned host record), allocated on
- *     first use and held until the process ends.  Its size does not depend on
- *     n (constant-size buffers, Sec. 6.2).
+ *     partial sums, one result record, a barrier counter, one pinned host
+ *     record: about 64 KiB of device memory), allocated on a stream's first
+ *     call and held until zero_stream_release(stream) or the process ends, so
+ *     the library's memory grows with the number of distinct streams it has
+ *     seen.  Its size does not depend on n (constant-size buffers, Sec. 6.2).
  *   - `stream` is a hipStream_t passed as void*; NULL is the null stream.  The
  *     device is the current HIP device of the calling thread; a stream of
  *     another device is rejected with ZERO_EINVAL.
  *   - Concurrent calls are serialised per (device, stream) by the library.
  *     The workspace is keyed by the stream handle: do not destroy a stream
- *     while calls on it are in flight (a new stream may reuse its handle).
+ *     while calls on it are in flight, and release its workspace
+ *     (zero_stream_release) before destroying a stream, since a new stream may
+ *     be handed the same handle.
  */
 #ifndef ZERO_SHARD_H
 #define ZERO_SHARD_H
@@ -105,7 +109,11 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
  * the vectorised path runs after a few scalar head elements).  Placement
  * affects speed, not results: separate allocations, or arrays packed into one
  * buffer each on its own 2 MiB boundary, run fastest; arrays offset from one
- * another by a few hundred bytes run about 5 % slower.  The call
+ * another by a few hundred bytes run about 5 % slower.  Shards of up to 2^22
+ * elements whose arrays share one misalignment take a single cooperative
+ * launch (statistics, a grid barrier and the update in one kernel, the
+ * gradient read once); larger ones take the statistics kernels and the update
+ * kernel.  The call
  * blocks until the skip decision is known (the statistics kernels publish it
  * in host-mapped memory, which the calling thread polls); the update kernel
  * may still be running on `stream` when it returns.  Returns 0 applied,
@@ -171,27 +179,34 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
 /* Resident step: the whole step, loss scaler included, driven by a state
  * record in DEVICE memory, so a call only enqueues kernels and never waits;
  * the enqueued work can be captured into a HIP graph and replayed, each replay
- * being the next optimizer step.  The caller owns the record: it writes the
- * hyperparameters and the scaler's starting values (host copy before the
- * first step, or between steps), and reads t / loss_scale / skipped whenever
- * it needs them.  Per step, on the device:
+ * being the next optimizer step.  The caller owns the record: it fills it with
+ * zero_resident_state_init (a host copy, checked there) and copies it to the
+ * device before the first step or between steps, and reads t / loss_scale /
+ * skipped whenever it needs them.  Per step, on the device:
  *   statistics of grad16 (as zero_shard_step) -> scalars from the record's
  *   loss_scale and clip -> the fp32 constants from lr, betas, eps, weight
  *   decay and t (each computed in double and rounded once, the bias
- *   corrections with the device's pow) -> the scaler: on a skip halve
- *   loss_scale (not below min_scale), good = 0; else t += 1, good += 1 and
- *   double loss_scale when good reaches window (> 0), good = 0 -> skip or the
- *   update.  The record is updated before the update kernel runs (which reads
- *   only the scalars and constants taken from it before); once the step's work
- *   on the stream is complete the record describes the step just taken.
- * Same arrays, checks and skip semantics as zero_shard_step.  The first call
- * on a stream allocates the stream's workspace, so make one call before
- * capturing; while the stream is capturing, the allocation checks and the
- * sampled timing (zero_profile_enable) are left out, so make an eager call
- * with the same arrays first.  `state` must be 8-byte aligned device memory
- * (or mapped host memory) that no array overlaps; its hyperparameters are the
- * caller's to keep in the ranges zero_shard_step accepts (the kernels do not
- * check them). */
+ *   corrections as zero_bias_corrections defines them) -> the scaler: on a
+ *   skip halve loss_scale (not below min_scale), good = 0; else t += 1,
+ *   good += 1 and double loss_scale when good reaches window (> 0), good = 0
+ *   -> skip or the update.  The record is updated before the update kernel
+ *   runs (which reads only the scalars and constants taken from it before);
+ *   once the step's work on the stream is complete the record describes the
+ *   step just taken.  A record whose hyperparameters are outside the ranges
+ *   zero_shard_step accepts (or min_scale not finite and > 0) is not a valid
+ *   step: nothing is written and only its `skipped` field changes, to -1.
+ * Workspace: each state record has its own (statistics partials, result
+ * record, constants; about 64 KiB of device memory), allocated on the first
+ * step taken with it and held until zero_resident_release(state) or the
+ * process ends.  Eager calls and graph replays with that record use it, and
+ * nothing else does; so steps with one record must not overlap each other
+ * (they also read and advance its t and loss scale), while steps with
+ * different records, graph replays included, may run concurrently on any
+ * streams.  Same arrays, checks and skip semantics as zero_shard_step.  Make
+ * one eager call with the arrays and the record before capturing: while the
+ * stream is capturing, the allocation checks and the sampled timing
+ * (zero_profile_enable) are left out.  `state` must be 8-byte aligned device
+ * memory (or mapped host memory) that no array overlaps. */
 typedef struct {
     double lr, beta1, beta2, eps, weight_decay, clip; /* hyperparameters (caller)          */
     double loss_scale;                                /* current loss scale                */
@@ -200,12 +215,29 @@ typedef struct {
     int64_t t;                                        /* t of the next applied update, >= 1 */
     int64_t good;                                     /* applied steps since skip or growth */
     int64_t steps;                                    /* steps taken, applied or skipped    */
-    int32_t skipped;                                  /* decision of the last step          */
+    int32_t skipped;                                  /* last step: 1 skipped, 0 applied,
+                                                         -1 record out of range             */
     int32_t pad_;
 } zero_resident_state_t;
 
+/* Fills a HOST record for the resident step after checking the values as
+ * zero_shard_step checks its arguments (lr, eps >= 0 finite, weight_decay
+ * finite, beta1, beta2 in [0, 1), t >= 1, loss_scale finite > 0, clip not
+ * NaN) and min_scale finite > 0; good, steps and skipped start at 0.
+ * ZERO_EINVAL (out untouched) otherwise. */
+int zero_resident_state_init(zero_resident_state_t* out, double lr, double beta1, double beta2, double eps,
+                             double weight_decay, double clip, double loss_scale, double min_scale, int64_t window,
+                             int64_t t);
+
 int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32, float* v32,
                              uint16_t* param16_out, int64_t n, zero_resident_state_t* state, void* stream);
+
+/* Frees the workspace the resident step holds for `state` on the current
+ * device (nothing to do if it holds none).  Graph replays may use it on any
+ * stream, so this first waits for the device to finish its queued work.  A
+ * later step with the record allocates a new workspace; graphs captured with
+ * it must not be replayed after the release.  Returns 0 or ZERO_EHIP. */
+int zero_resident_release(const zero_resident_state_t* state);
 
 /* The array checks of zero_shard_step without launching anything: n range,
  * NULL pointers, alignment, that each array [p, p + n*size) lies inside one
@@ -220,7 +252,8 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
 int zero_shard_validate(const uint16_t* grad16, const float* master32, const float* m32, const float* v32,
                         const uint16_t* param16_out, int64_t n);
 
-/* Statistics of the calling thread's last successful zero_shard_step. */
+/* Statistics of the calling thread's last successful zero_shard_step (or
+ * zero_lamb_step). */
 typedef struct {
     double sumsq;     /* sum of grad16^2 (loss-scaled), accumulated in fp64;
                          non-finite iff overflow                                  */
@@ -229,13 +262,33 @@ typedef struct {
     float mult;       /* fp32 multiplier applied to grad16: (float)(coef/scale)   */
     int32_t overflow; /* 1 if any grad16 element was inf or NaN                   */
     int32_t skipped;  /* equals overflow                                          */
-    int32_t pad_;
+    int32_t path;     /* 1: the one-launch small-shard step; 0: statistics kernels
+                         and update kernel                                        */
     int64_t n;        /* elements of that call                                    */
 } zero_step_stats_t;
 
-/* Copies the last step's statistics; ZERO_EINVAL if out is NULL or this
- * thread has made no successful zero_shard_step call yet. */
-int zero_shard_last_stats(zero_step_stats_t* out);
+/* The clipping diagnostics of the calling thread's last successful step
+ * (Sec. 3.2: the norm over the gradient; the clipping multiplier and the
+ * overflow flag of the mixed-precision step): *norm = sqrt(sum grad16^2) /
+ * loss_scale (+inf on overflow), *mult = the fp32 multiplier applied to
+ * grad16, *overflow = 1 if some element was inf or NaN.  Host pointers; any
+ * of them may be NULL (not all three).  ZERO_EINVAL if all are NULL or this
+ * thread has made no successful step yet. */
+int zero_shard_last_stats(double* norm, float* mult, int* overflow);
+
+/* The same step's whole record (sum of squares, norm, clipping coefficient,
+ * multiplier, overflow, skip flag, n) into *out (host); ZERO_EINVAL if out is
+ * NULL or this thread has made no successful step yet. */
+int zero_shard_last_step_stats(zero_step_stats_t* out);
+
+/* The fp32 bias corrections 1 - beta1^t and 1 - beta2^t that every Adam and
+ * LAMB update uses (Adam's bias-corrected moments, Kingma & Ba, cited in
+ * Sec. 3.1): beta^t is the double nearest the exact power, 1 - beta^t is
+ * taken in double and rounded once to fp32.  The host calls and the resident
+ * step's kernel evaluate this one definition and get the same bits.  Host
+ * only (no GPU needed).  beta1, beta2 in [0, 1), step >= 1, bc1 and bc2
+ * non-NULL host pointers, else ZERO_EINVAL. */
+int zero_bias_corrections(double beta1, double beta2, int64_t step, float* bc1, float* bc2);
 
 /* ------------------------------------------------------------------------ */
 /* Dynamic loss scaling (host state owned by the caller)                     */
@@ -265,9 +318,19 @@ int zero_scaler_update(zero_scaler_t* s, int32_t skipped);
 #define ZERO_STAGE_OS_G 2     /* 2*Psi + (2 + K)*Psi/N_d         */
 #define ZERO_STAGE_OS_G_P 3   /* (2 + 2 + K)*Psi/N_d             */
 
-/* Bytes of model state per device for psi parameters at data-parallel degree
- * nd (> 0) and optimizer-state multiplier k (12 for mixed-precision Adam).
- * ZERO_EINVAL for an unknown stage, nd <= 0, psi < 0 or out == NULL. */
+/* Bytes of model state per device (Sec. 3.1: fp16 parameters and gradients
+ * take 2 bytes each per parameter and the optimizer state K bytes, K = 12 for
+ * mixed-precision Adam; Sec. 5.1-5.3 and Table 1: P_os divides the optimizer
+ * state by N_d, P_os+g also the gradients, P_os+g+p everything) for psi
+ * parameters, data-parallel degree nd >= 1 and multiplier k >= 0 (bytes per
+ * parameter of optimizer state), written to *bytes (host).  Evaluated in
+ * double; psi >= 0 and finite.  ZERO_EINVAL for an unknown stage, nd < 1,
+ * k < 0, a bad psi or bytes == NULL. */
+int zero_memory_bytes(double psi, int32_t nd, int32_t stage, int32_t k, double* bytes);
+
+/* zero_memory_bytes with nd and k as doubles (fractional K for optimizers whose
+ * state is not a whole number of bytes per parameter): nd > 0 and k finite,
+ * psi >= 0 finite, else ZERO_EINVAL. */
 int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, double* out);
 
 /* ------------------------------------------------------------------------ */
@@ -295,11 +358,12 @@ int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, doubl
  * shard; its norms then need the split-phase calls below.  The plan is tied to
  * the device current at creation and owns device memory (about 16 bytes per
  * 256 elements plus 32 bytes per layer, and the work lists, built per array
- * alignment on first use); zero_lamb_plan_destroy waits for the device and
- * frees it.  Calls on one plan are serialised by the library; a call on a
- * different stream from the plan's previous call first waits for the device
- * to finish its queued work (hipDeviceSynchronize), so keep a plan on one
- * stream in a loop.
+ * alignment on first use); zero_lamb_plan_destroy waits for the plan's own
+ * queued work and frees it.  Calls on one plan are serialised by the library:
+ * each call records a plan-owned event after its kernels, and a call on a
+ * different stream from the plan's previous one makes its stream wait for
+ * that event on the device (no host wait, no other stream affected; the
+ * event stays valid if the previous stream has been destroyed).
  * Returns ZERO_OK, ZERO_EINVAL (bad table, n outside [0, 2^40], NULL out) or
  * ZERO_ENOMEM / ZERO_EHIP. */
 typedef struct zero_lamb_plan zero_lamb_plan_t;
@@ -341,7 +405,7 @@ int zero_lamb_apply(const zero_lamb_plan_t* plan, float* master32, const float* 
  * one zero_profile_enable sets): events before the statistics, moments,
  * layer-sum and apply kernels and after the last.  zero_lamb_profile_read
  * waits for the recorded work, returns the sums since the last read and resets
- * them. */
+ * them; a deferred profiling failure is reported as by zero_profile_read. */
 typedef struct {
     int64_t steps;      /* steps timed                                  */
     double stats_ms;    /* statistics + finalize kernels                */
@@ -361,14 +425,19 @@ int zero_lamb_profile_read(zero_lamb_profile_t* out);
 const char* zero_last_error(void);
 
 /* Kernel timing with HIP events on the call's own stream.  With every = k > 0,
- * one zero_shard_step in k on each stream records events before its
- * statistics kernels, before its update kernel and after it (each event marker
- * costs the GPU a few microseconds, hence the sampling); zero_shard_apply and
- * zero_shard_apply_async calls are sampled the same way, their statistics
- * interval covering only the result-record kernel; every = 0 disables.
- * zero_profile_read waits for the recorded work, then returns the summed
- * durations and the number of profiled steps since enabling (or the last read)
- * and resets them.  ZERO_EINVAL for every < 0. */
+ * one zero_shard_step in k on each stream records its own three events:
+ * before its statistics kernels, before its update kernel and after it (each
+ * event marker costs the GPU a few microseconds, hence the sampling; for the
+ * one-launch small-shard step the whole kernel counts as the update);
+ * zero_shard_apply, zero_shard_apply_async and eager resident calls are
+ * sampled the same way, their statistics interval covering only the
+ * one-workgroup kernel; every = 0 disables.  zero_profile_read waits for the
+ * recorded work, then returns the summed durations and the number of
+ * profiled steps since enabling (or the last read) and resets them.  A
+ * profiling failure after a step's kernels were queued never fails that step:
+ * the sample is dropped and the next zero_profile_read returns ZERO_EHIP with
+ * the message (the totals of the other samples are still written).
+ * ZERO_EINVAL for every < 0. */
 typedef struct {
     int64_t steps;      /* steps timed                                        */
     double stats_ms;    /* total time of the statistics + finalize kernels    */
@@ -378,12 +447,39 @@ typedef struct {
 int zero_profile_enable(int32_t every);
 int zero_profile_read(zero_profile_t* out);
 
+/* Frees the per-(device, stream) workspace of `stream` on the current device
+ * after waiting for the work queued on that stream (nothing to do if the
+ * library holds none for it).  Call it before destroying a stream the library
+ * has been used on; a later call on the stream allocates a new workspace.
+ * Calls on the stream from other threads wait for the release or run on a
+ * fresh workspace, never on freed memory.  Returns 0, ZERO_EINVAL (a stream of
+ * another device) or ZERO_EHIP. */
+int zero_stream_release(void* stream);
+
+/* The number of per-stream workspaces and of resident-record workspaces the
+ * library holds (all devices), for leak checks; either pointer may be NULL
+ * (not both). */
+int zero_workspace_count(int64_t* streams, int64_t* records);
+
 /* Device-to-device copy of `bytes` bytes with the library's own streaming
  * kernel (16-byte vectors): the achievable-bandwidth reference for the update
  * kernel and the calibration kernel for hardware byte counters.  src and dst
  * must be 16-byte aligned, bytes a multiple of 16, ranges disjoint, each inside
  * one GPU-accessible allocation; ZERO_EINVAL otherwise, before any launch. */
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
+/* Byte-mix probes of the LAMB passes: one launch over the shard's arrays with
+ * the launch shape, tile walk, vector width and cache policy of
+ * k_lamb_moments (pass 0: reads grad16, master32, m32, v32; writes m32, v32)
+ * or k_lamb_apply (pass 1: reads master32, m32, v32; writes master32,
+ * param16_out), doing one or two adds per element instead of the pass's
+ * arithmetic: the achievable time of that pass's streams on this device.
+ * The arrays it writes get meaningless values.  fp32 arrays 16-byte aligned,
+ * fp16 arrays 8-byte aligned (the array a pass does not touch may be NULL),
+ * each inside one GPU allocation, no overlaps; ZERO_EINVAL otherwise, before
+ * any launch.  Enqueues only. */
+int zero_probe_lamb_pass(int32_t pass, const uint16_t* grad16, float* master32, float* m32, float* v32,
+                         uint16_t* param16_out, int64_t n, void* stream);
 
 #ifdef __cplusplus
 }

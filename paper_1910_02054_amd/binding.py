@@ -33,7 +33,7 @@ class Layout(ctypes.Structure):
 class StepStats(ctypes.Structure):
     _fields_ = [("sumsq", ctypes.c_double), ("norm", ctypes.c_double), ("coef", ctypes.c_double),
                 ("mult", ctypes.c_float), ("overflow", ctypes.c_int32), ("skipped", ctypes.c_int32),
-                ("pad_", ctypes.c_int32), ("n", ctypes.c_int64)]
+                ("path", ctypes.c_int32), ("n", ctypes.c_int64)]
 
 
 class ScalerState(ctypes.Structure):
@@ -64,7 +64,17 @@ _lib.zero_shard_step.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _db
 _lib.zero_shard_stats.argtypes = [_P, _i64, ctypes.POINTER(_dbl), _P]
 _lib.zero_shard_apply.argtypes = [_P, _P, _P, _P, _P, _i64, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
 _lib.zero_shard_validate.argtypes = [_P, _P, _P, _P, _P, _i64]
-_lib.zero_shard_last_stats.argtypes = [ctypes.POINTER(StepStats)]
+_lib.zero_shard_last_stats.argtypes = [ctypes.POINTER(_dbl), ctypes.POINTER(ctypes.c_float),
+                                       ctypes.POINTER(ctypes.c_int)]
+_lib.zero_shard_last_step_stats.argtypes = [ctypes.POINTER(StepStats)]
+_lib.zero_memory_bytes.argtypes = [_dbl, _i32, _i32, _i32, ctypes.POINTER(_dbl)]
+_lib.zero_bias_corrections.argtypes = [_dbl, _dbl, _i64, ctypes.POINTER(ctypes.c_float),
+                                       ctypes.POINTER(ctypes.c_float)]
+_lib.zero_resident_state_init.argtypes = [_P, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _i64]
+_lib.zero_resident_release.argtypes = [_P]
+_lib.zero_stream_release.argtypes = [_P]
+_lib.zero_workspace_count.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
+_lib.zero_probe_lamb_pass.argtypes = [_i32, _P, _P, _P, _P, _P, _i64, _P]
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
 _lib.zero_model_state_bytes.argtypes = [_dbl, _dbl, _i32, _dbl, ctypes.POINTER(_dbl)]
@@ -83,20 +93,17 @@ _lib.zero_lamb_step.argtypes = [_P, _P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, 
 _lib.zero_lamb_moments.argtypes = [_P, _P, _P, _P, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P, _P]
 _lib.zero_lamb_apply.argtypes = [_P, _P, _P, _P, _P, _dbl, _P, _dbl, _dbl, _dbl, _dbl, _dbl, _i64, _dbl, _dbl, _P]
 _lib.zero_lamb_profile_read.argtypes = [ctypes.POINTER(LambProfile)]
-for _f in ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
-           "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
-           "zero_scaler_update", "zero_model_state_bytes", "zero_profile_enable", "zero_profile_read",
-           "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step",
-           "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async",
-           "zero_shard_apply_async", "zero_shard_step_resident"):
-    getattr(_lib, _f).restype = ctypes.c_int
-
 EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero_shard_apply",
-           "zero_shard_validate", "zero_shard_last_stats", "zero_scaler_init",
-           "zero_scaler_update", "zero_model_state_bytes", "zero_last_error", "zero_profile_enable",
-           "zero_profile_read", "zero_probe_copy", "zero_lamb_plan_create", "zero_lamb_plan_destroy",
-           "zero_lamb_step", "zero_lamb_moments", "zero_lamb_apply", "zero_lamb_profile_read",
-           "zero_shard_stats_async", "zero_shard_apply_async", "zero_shard_step_resident")
+           "zero_shard_validate", "zero_shard_last_stats", "zero_shard_last_step_stats", "zero_scaler_init",
+           "zero_scaler_update", "zero_memory_bytes", "zero_model_state_bytes", "zero_bias_corrections",
+           "zero_last_error", "zero_profile_enable", "zero_profile_read", "zero_probe_copy",
+           "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step", "zero_lamb_moments",
+           "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async", "zero_shard_apply_async",
+           "zero_resident_state_init", "zero_shard_step_resident", "zero_resident_release",
+           "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass")
+for _f in EXPORTS:
+    if _f != "zero_last_error":
+        getattr(_lib, _f).restype = ctypes.c_int
 
 
 def _check(rc):
@@ -232,14 +239,41 @@ def zero_shard_apply_async(grad16, master32, m32, v32, param16_out, global_sumsq
         _addr(skipped, (torch.int32,), "skipped"), _stream(stream)))
 
 
+def resident_state_record(lr, beta1, beta2, eps, weight_decay, clip, loss_scale, min_scale=1.0, window=1000,
+                          t=1) -> ResidentState:
+    """A host zero_resident_state_t filled (and checked) by zero_resident_state_init."""
+    st = ResidentState()
+    _check(_lib.zero_resident_state_init(ctypes.addressof(st), float(lr), float(beta1), float(beta2), float(eps),
+                                         float(weight_decay), float(clip), float(loss_scale), float(min_scale),
+                                         int(window), int(t)))
+    return st
+
+
 def resident_state(device, lr, beta1, beta2, eps, weight_decay, clip, loss_scale, min_scale=1.0, window=1000, t=1):
     """A zero_resident_state_t record in device memory (a uint8 torch tensor), initialised
-    from the host."""
+    from the host by zero_resident_state_init (which rejects out-of-range values)."""
     import torch
-    st = ResidentState(lr=lr, beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay, clip=clip,
-                       loss_scale=loss_scale, min_scale=min_scale, window=window, t=t, good=0, steps=0, skipped=0)
+    st = resident_state_record(lr, beta1, beta2, eps, weight_decay, clip, loss_scale, min_scale, window, t)
     host = torch.frombuffer(bytearray(bytes(st)), dtype=torch.uint8)
     return host.to(device)
+
+
+def zero_resident_release(state):
+    """Free the resident step's workspace held for `state` (a device record tensor or address)."""
+    _check(_lib.zero_resident_release(_addr(state, None, "state")))
+
+
+def zero_stream_release(stream=None):
+    """Free the library's workspace of `stream` (torch stream, raw handle, or None for the
+    current stream) after its queued work."""
+    _check(_lib.zero_stream_release(_stream(stream)))
+
+
+def zero_workspace_count():
+    """(per-stream workspaces, resident-record workspaces) the library holds."""
+    a, b = _i64(), _i64()
+    _check(_lib.zero_workspace_count(ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
 
 
 def read_resident_state(state_tensor) -> ResidentState:
@@ -270,10 +304,25 @@ def zero_shard_validate(grad16, master32, m32, v32, param16_out, n):
                                            _addr(param16_out), int(n)))
 
 
-def zero_shard_last_stats() -> StepStats:
+def zero_shard_last_stats():
+    """(norm, mult, overflow) of the calling thread's last successful step."""
+    norm, mult, ovf = _dbl(), ctypes.c_float(), ctypes.c_int()
+    _check(_lib.zero_shard_last_stats(ctypes.byref(norm), ctypes.byref(mult), ctypes.byref(ovf)))
+    return norm.value, mult.value, ovf.value
+
+
+def zero_shard_last_step_stats() -> StepStats:
+    """The whole statistics record of the calling thread's last successful step."""
     out = StepStats()
-    _check(_lib.zero_shard_last_stats(ctypes.byref(out)))
+    _check(_lib.zero_shard_last_step_stats(ctypes.byref(out)))
     return out
+
+
+def zero_bias_corrections(beta1, beta2, step):
+    """The fp32 bias corrections (1 - beta1^t, 1 - beta2^t) the update kernels use (host only)."""
+    a, b = ctypes.c_float(), ctypes.c_float()
+    _check(_lib.zero_bias_corrections(float(beta1), float(beta2), int(step), ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
 
 
 class Scaler:
@@ -293,6 +342,12 @@ class Scaler:
 
     def update(self, skipped):
         _check(_lib.zero_scaler_update(ctypes.byref(self.state), 1 if skipped else 0))
+
+
+def zero_memory_bytes(psi: float, nd: int, stage: int, k: int = 12) -> float:
+    out = ctypes.c_double()
+    _check(_lib.zero_memory_bytes(float(psi), int(nd), int(stage), int(k), ctypes.byref(out)))
+    return out.value
 
 
 def zero_model_state_bytes(psi: float, nd: float, stage: int, k: float = 12.0) -> float:
@@ -323,6 +378,14 @@ def zero_probe_copy(src, dst, nbytes=None, stream=None):
         if not isinstance(t, int) and t.numel() * t.element_size() < nbytes:
             raise ValueError("nbytes = %d exceeds a buffer of %d bytes" % (nbytes, t.numel() * t.element_size()))
     _check(_lib.zero_probe_copy(_addr(src), _addr(dst), int(nbytes), _stream(stream)))
+
+
+def zero_probe_lamb_pass(pass_, grad16, master32, m32, v32, param16_out, n=None, stream=None):
+    """Enqueue the byte-mix probe of LAMB pass `pass_` (0 moments, 1 apply) over the arrays
+    (it overwrites what that pass writes)."""
+    n = _shard_len(n, *(a for a in (grad16, master32, m32, v32, param16_out) if a is not None))
+    _check(_lib.zero_probe_lamb_pass(int(pass_), _addr(grad16), _addr(master32), _addr(m32), _addr(v32),
+                                     _addr(param16_out), int(n), _stream(stream)))
 
 
 class LambPlan:

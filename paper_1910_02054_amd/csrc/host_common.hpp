@@ -7,6 +7,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <memory>
 #include <mutex>
 #include <string>
 
@@ -33,26 +34,57 @@ int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 
 constexpr int64_t kMaxNumel = (int64_t)1 << 40;
 
+// Per-device launch facts, computed once per device (no allocation): compute
+// units and the dynamic-LDS reservations that cap resident workgroups of the
+// streaming kernels (occupancy_lds).
+struct DevInfo {
+    int ncu = 0;
+    size_t stats_lds = 0, adam_lds = 0;
+    int stats_resident = 0, adam_resident = 0;
+    int64_t small_cap[4] = {0, 0, 0, 0};  // co-resident workgroups of k_small_step<1, 2, 4, 8>
+                                          // (0: no cooperative launch on this device)
+};
+
+// The facts of device `dev` (0 <= dev < kMaxDevices), filled on first use.
+int dev_info(int dev, const DevInfo** out);
+constexpr int kMaxDevices = 64;
+
 // Per-(device, stream) context: the constant-size workspace of the gradient
-// statistics and the result record the update kernels read.
+// statistics and the result record the update kernels read.  A context is
+// shared (std::shared_ptr) between the registry and the calls using it, so a
+// release (zero_stream_release) never frees memory under a running call: the
+// releasing thread takes `mu`, waits for the stream, frees the device buffers
+// and marks the context released; a call that locks it afterwards sees the
+// mark and takes a fresh context.
 struct Ctx {
     std::mutex mu;
+    int dev = 0;
+    hipStream_t stream = nullptr;
     zs::Partial* part = nullptr;    // kMaxStatsBlocks partial records (device)
     zs::Result* res = nullptr;      // result record (device), read by the update kernel
     zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
     zs::Result* host_dev = nullptr; // its device-side address
-    zs::AdamConst* dconst = nullptr; // fp32 constants of the resident step (device)
-    hipEvent_t prof_last_end = nullptr;  // end event of the last profiled update on this stream
-    uint64_t prof_tick = 0;              // steps seen while profiling (for sampling)
+    uint64_t* bar = nullptr;        // grid-barrier counter of the small-shard step (device)
+    uint64_t bar_count = 0;         // arrivals the counter has received so far
+    bool bar_ready = false;         // the counter has been zeroed on the stream
+    uint64_t prof_tick = 0;         // steps seen while profiling (for sampling)
+    uint64_t prof_epoch = 0;        // profiling period the tick belongs to
     uint32_t seq = 0;               // call counter echoed in the result record
-    int ncu = 0;
-    size_t stats_lds = 0, adam_lds = 0;   // occupancy reservations (dynamic LDS per workgroup)
-    int stats_resident = 0, adam_resident = 0;
+    bool released = false;
+    const DevInfo* info = nullptr;
 };
 
-// The context of (current device, stream), created on first use; rejects a
-// stream of another device.
-int get_ctx(hipStream_t stream, Ctx** out);
+// A context of (current device, stream), locked for the duration of a call.
+struct CtxLock {
+    std::shared_ptr<Ctx> ref;
+    std::unique_lock<std::mutex> lk;
+    Ctx* operator->() const { return ref.get(); }
+    Ctx* get() const { return ref.get(); }
+};
+
+// The locked context of (current device, stream), created on first use;
+// rejects a stream of another device.
+int lock_ctx(hipStream_t stream, CtxLock* out);
 
 // Next call sequence number of a context (never 0).  Caller holds ctx->mu.
 uint32_t next_seq(Ctx* ctx);
@@ -85,5 +117,14 @@ int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out);
 
 // Sampling period of kernel profiling (0 = off), set by zero_profile_enable.
 int prof_every();
+
+// Records a profiling failure that happened after a step's kernels were
+// queued (slot 0: Adam steps, read by zero_profile_read; slot 1: LAMB steps,
+// read by zero_lamb_profile_read), so the step itself does not fail.
+void prof_defer_error(int slot, const char* what, hipError_t e);
+
+// The deferred profiling error of `slot` as a return code (0 if none), its
+// message moved to zero_last_error; clears the slot.
+int prof_take_error(int slot);
 
 }  // namespace zsh

@@ -365,4 +365,58 @@ __global__ __launch_bounds__(BLOCK) void k_lamb_apply(float* __restrict__ th, co
     }
 }
 
+// ---------------------------------------------------------------------------
+// Byte-mix probes of the two passes: the same arrays, tile walk (XCD-contiguous
+// tiles of 4*BLOCK*U elements, one tile per workgroup), vector width and cache
+// policy as k_lamb_moments (PASS 0: reads g16, theta, m, v; writes m, v) and
+// k_lamb_apply (PASS 1: reads theta, m, v; writes theta, p16), with one or two
+// adds per element in place of the pass's arithmetic and no work lists.  Their
+// time is the achievable time of each pass's streams at its launch shape.
+// Arrays 16-byte aligned (fp16 8-byte); the last partial vector is scalar.
+// ---------------------------------------------------------------------------
+template <int BLOCK, int U, bool NTL, bool NTS, bool XCD, int PASS>
+__global__ __launch_bounds__(BLOCK) void k_probe_lamb(const uint16_t* __restrict__ g, float* __restrict__ th,
+                                                      float* __restrict__ m, float* __restrict__ v,
+                                                      uint16_t* __restrict__ p, int64_t ntiles, int64_t n) {
+    constexpr int64_t T = 4 * (int64_t)BLOCK * U;
+    for (int64_t b = logical_block<XCD>(); b < ntiles; b += gridDim.x) {
+        const int64_t te = (b + 1) * T < n ? (b + 1) * T : n;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t e0 = b * T + 4 * ((int64_t)threadIdx.x + (int64_t)u * BLOCK);
+            if (e0 + 4 <= te) {
+                if constexpr (PASS == 0) {
+                    const u32x2 gq = ld<NTL>(reinterpret_cast<const u32x2*>(g + e0));
+                    const f32x4 tq = ld<NTL>(reinterpret_cast<const f32x4*>(th + e0));
+                    const f32x4 mq = ld<NTL>(reinterpret_cast<const f32x4*>(m + e0));
+                    const f32x4 vq = ld<NTL>(reinterpret_cast<const f32x4*>(v + e0));
+                    const f32x4 gf = {f16_to_f32(gq.x & 0xFFFFu), f16_to_f32(gq.x >> 16), f16_to_f32(gq.y & 0xFFFFu),
+                                      f16_to_f32(gq.y >> 16)};
+                    st<NTS>(mq + gf, reinterpret_cast<f32x4*>(m + e0));
+                    st<NTS>(vq + tq, reinterpret_cast<f32x4*>(v + e0));
+                } else {
+                    const f32x4 tq = ld<NTL>(reinterpret_cast<const f32x4*>(th + e0));
+                    const f32x4 mq = ld<NTL>(reinterpret_cast<const f32x4*>(m + e0));
+                    const f32x4 vq = ld<NTL>(reinterpret_cast<const f32x4*>(v + e0));
+                    const f32x4 o = tq + mq + vq;
+                    st<NTS>(o, reinterpret_cast<f32x4*>(th + e0));
+                    st<NTS>(u32x2{f32_to_f16(o.x) | (f32_to_f16(o.y) << 16), f32_to_f16(o.z) | (f32_to_f16(o.w) << 16)},
+                            reinterpret_cast<u32x2*>(p + e0));
+                }
+            } else {
+                for (int64_t i = e0; i < te && i < e0 + 4; ++i) {
+                    if constexpr (PASS == 0) {
+                        m[i] = m[i] + f16_to_f32(g[i]);
+                        v[i] = v[i] + th[i];
+                    } else {
+                        const float o = th[i] + m[i] + v[i];
+                        th[i] = o;
+                        p[i] = (uint16_t)f32_to_f16(o);
+                    }
+                }
+            }
+        }
+    }
+}
+
 }  // namespace zs

@@ -18,6 +18,11 @@
 //               device memory and to a host-mapped record.
 //   k_adam_*    the fused update: unscale+clip, Adam with bias correction, fp16
 //               cast; 14 bytes read and 14 bytes written per element.
+// Small shards take one cooperative launch instead (k_small_step): every
+// thread keeps its elements in registers, the workgroups meet at a grid
+// barrier after the statistics, each totals the partials in the same fixed
+// order, and the update follows from the registers (28 bytes per element, one
+// launch).
 // The other ways of running the same step swap only the one-thread kernels
 // around these: the split phase takes the global sum from the host
 // (k_set_result) or from device memory (k_finalize_sum writes a rank's local
@@ -29,7 +34,8 @@
 // Numerics: every fp32 operation of the update is correctly rounded (IEEE
 // division and square root, no contraction), in the order Adam's bias-corrected
 // form is written, so an element's result depends only on its own inputs and
-// the shared scalars.
+// the shared scalars.  The bias corrections 1 - beta^t come from one
+// definition shared by the host and the device (bias_correction below).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -98,10 +104,82 @@ struct alignas(16) Result {
     int32_t unused[2];
 };
 
-// fp32 constants of the update, each rounded once from a double on the host.
+// fp32 constants of the update, each rounded once from a double (on the host,
+// or on the device for the resident step).
 struct AdamConst {
     float lr, b1, omb1, b2, omb2, bc1, bc2, eps, wd;
 };
+
+// beta^t for an integer t >= 0, as the double nearest the exact power.  Binary
+// powering in double-double arithmetic: each product's rounding error is
+// recovered exactly with a fused multiply-add, so the pair carries the power to
+// about 2^-90 relative error before the one final rounding to double (the
+// exact power of a double is never a midpoint between doubles for t >= 2).
+// Every operation is a correctly rounded IEEE multiply, add or fused
+// multiply-add, so the host and the device compute the same bits.
+struct DDouble {
+    double hi, lo;
+};
+
+__host__ __device__ inline DDouble dd_mul(DDouble a, DDouble b) {
+    const double p = a.hi * b.hi;
+    double e = __builtin_fma(a.hi, b.hi, -p);
+    e = e + (a.hi * b.lo + a.lo * b.hi);
+    const double s = p + e;
+    return DDouble{s, e - (s - p)};
+}
+
+__host__ __device__ inline double pow_int(double b, int64_t t) {
+    DDouble r{1.0, 0.0}, x{b, 0.0};
+    while (t > 0) {
+        if (t & 1)
+            r = dd_mul(r, x);
+        t >>= 1;
+        if (t)
+            x = dd_mul(x, x);
+    }
+    return r.hi;
+}
+
+// The fp32 bias correction 1 - beta^t of Adam's moment estimates: the power
+// rounded to double, the difference in double, then one rounding to fp32.
+__host__ __device__ inline float bias_correction(double beta, int64_t t) {
+    return (float)(1.0 - pow_int(beta, t));
+}
+
+// The fp32 constants from the hyperparameters (each computed in double and
+// rounded once).
+__host__ __device__ inline AdamConst make_adam_const(double lr, double beta1, double beta2, double eps, double wd,
+                                                     int64_t t) {
+    AdamConst c;
+    c.lr = (float)lr;
+    c.b1 = (float)beta1;
+    c.omb1 = (float)(1.0 - beta1);
+    c.b2 = (float)beta2;
+    c.omb2 = (float)(1.0 - beta2);
+    c.bc1 = bias_correction(beta1, t);
+    c.bc2 = bias_correction(beta2, t);
+    c.eps = (float)eps;
+    c.wd = (float)wd;
+    return c;
+}
+
+// The hyperparameter ranges every step accepts (the synchronous entry points
+// check the same on the host): lr, eps >= 0 and finite, weight decay finite,
+// beta1, beta2 in [0, 1), t >= 1, loss scale finite and > 0, clip not NaN.
+__host__ __device__ inline bool hyper_ok(double lr, double beta1, double beta2, double eps, double wd, int64_t t,
+                                         double loss_scale, double clip) {
+    return __builtin_isfinite(lr) && lr >= 0.0 && __builtin_isfinite(eps) && eps >= 0.0 && __builtin_isfinite(wd) &&
+           beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0 && t >= 1 && __builtin_isfinite(loss_scale) &&
+           loss_scale > 0.0 && !__builtin_isnan(clip);
+}
+
+// A resident state record the step can run from: hyper_ok plus a finite
+// min_scale > 0.
+__host__ __device__ inline bool resident_record_ok(const zero_resident_state_t& s) {
+    return hyper_ok(s.lr, s.beta1, s.beta2, s.eps, s.weight_decay, s.t, s.loss_scale, s.clip) &&
+           __builtin_isfinite(s.min_scale) && s.min_scale > 0.0;
+}
 
 __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
@@ -263,6 +341,12 @@ __device__ __forceinline__ double partials_total(const Partial* __restrict__ par
         *out = value;
 }
 
+// One 64-bit word into device memory (a counter cleared in stream order).
+[[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_u64(uint64_t* __restrict__ out, uint64_t value) {
+    if (threadIdx.x == 0)
+        *out = value;
+}
+
 // Statistics total into caller device memory (the asynchronous split phase:
 // no result record, no host copy).
 [[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_finalize_sum(
@@ -294,43 +378,43 @@ __device__ __forceinline__ double partials_total(const Partial* __restrict__ par
 // Resident step, before the update, in one workgroup: the statistics total
 // (as k_finalize forms it), the result record from it and the state record's
 // loss scale and clip, the fp32 constants from the record's hyperparameters
-// and t (each computed in double and rounded once), and then the loss-scale
+// and t (make_adam_const, the host's definition), and then the loss-scale
 // schedule on the record: after an overflow the scale halves (not below
 // min_scale) and t stays; otherwise t and the good-step count advance and the
 // scale doubles after `window` good steps.  The update kernel reads only the
-// result record and the constants, so the schedule need not wait for it.
+// result record and the constants, so the schedule need not wait for it.  A
+// record outside the accepted ranges (resident_record_ok) is left unchanged
+// except for skipped = -1, and the step writes nothing.
 [[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_resident_begin(
     const Partial* __restrict__ part, int nparts, zero_resident_state_t* __restrict__ st, Result* __restrict__ res,
     AdamConst* __restrict__ cout, uint32_t seq) {
     const double tot = partials_total(part, nparts);
     if (threadIdx.x == 0) {
-        const Result r = make_result(tot, st->loss_scale, st->clip, seq);
+        const zero_resident_state_t s = *st;
+        if (!resident_record_ok(s)) {
+            Result r = make_result(0.0, 1.0, 0.0, seq);
+            r.skip = 1;
+            *res = r;
+            st->skipped = -1;
+            return;
+        }
+        const Result r = make_result(tot, s.loss_scale, s.clip, seq);
         *res = r;
-        const double t = (double)st->t;
-        AdamConst c;
-        c.lr = (float)st->lr;
-        c.b1 = (float)st->beta1;
-        c.omb1 = (float)(1.0 - st->beta1);
-        c.b2 = (float)st->beta2;
-        c.omb2 = (float)(1.0 - st->beta2);
-        c.bc1 = (float)(1.0 - pow(st->beta1, t));
-        c.bc2 = (float)(1.0 - pow(st->beta2, t));
-        c.eps = (float)st->eps;
-        c.wd = (float)st->weight_decay;
-        *cout = c;
-        st->steps += 1;
+        *cout = make_adam_const(s.lr, s.beta1, s.beta2, s.eps, s.weight_decay, s.t);
+        st->steps = s.steps + 1;
         st->skipped = r.skip;
         if (r.skip) {
-            const double h = st->loss_scale * 0.5;
-            st->loss_scale = h > st->min_scale ? h : st->min_scale;
+            const double h = s.loss_scale * 0.5;
+            st->loss_scale = h > s.min_scale ? h : s.min_scale;
             st->good = 0;
         } else {
-            st->t += 1;
-            st->good += 1;
-            if (st->window > 0 && st->good >= st->window) {
-                st->loss_scale *= 2.0;
-                st->good = 0;
+            st->t = s.t + 1;
+            int64_t good = s.good + 1;
+            if (s.window > 0 && good >= s.window) {
+                st->loss_scale = s.loss_scale * 2.0;
+                good = 0;
             }
+            st->good = good;
         }
     }
 }
@@ -463,6 +547,147 @@ __global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
     const int64_t stride = (int64_t)gridDim.x * kScalarBlock;
     for (int64_t i = (int64_t)blockIdx.x * kScalarBlock + threadIdx.x; i < n; i += stride)
         adam_one(g, th, m, v, p, i, mult, c);
+}
+
+// ---------------------------------------------------------------------------
+// One-launch small-shard step (cooperative launch: every workgroup of the grid
+// is resident at once, which the grid barrier below relies on).  The shard's
+// vector layout is k_adam_vec's (`head` scalar elements, `nvec` 4-element
+// vectors, a tail of 0..3); workgroup b owns vectors (b*V + u)*kSmallBlock +
+// threadIdx.x for u < V, so consecutive lanes touch consecutive vectors.
+//   1. Load the thread's gradient vectors, sum their exact squares in fp64,
+//      reduce over the workgroup (workgroup 0 also takes the head and tail
+//      elements) and store the workgroup's partial part[b].
+//   2. Arrive at the barrier (a release increment of *bar), then issue the
+//      loads of theta, m and v, which overlap the wait.
+//   3. Wait until *bar reaches bar_target (the host passes the count of
+//      arrivals this counter had received before the launch plus the grid
+//      size).  The wait is bounded: a workgroup that gives up writes nothing,
+//      and workgroup 0 then does not publish the record, so the host's wait
+//      ends with an error once the stream is idle.
+//   4. Every workgroup totals part[0, gridDim.x) in the same fixed order, so
+//      all of them hold the same bits; workgroup 0 publishes the result record
+//      (device and host-mapped, as k_finalize does).
+//   5. Unless the step is skipped, the update from the registers.
+// ---------------------------------------------------------------------------
+constexpr int kSmallBlock = 256;
+constexpr uint32_t kBarrierSpinLimit = 1u << 22;  // polls of about 0.1-1 us each
+
+template <int V>
+__global__ __launch_bounds__(kSmallBlock) void k_small_step(
+    const uint16_t* __restrict__ g, float* __restrict__ th, float* __restrict__ m, float* __restrict__ v,
+    uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec, double* __restrict__ part,
+    uint64_t* __restrict__ bar, uint64_t bar_target, Result* __restrict__ res, Result* __restrict__ res_host,
+    double loss_scale, double clip, uint32_t seq, AdamConst c) {
+    __shared__ float s_mult;
+    __shared__ int s_skip;
+    const u32x2* __restrict__ gv = reinterpret_cast<const u32x2*>(g + head);
+    f32x4* __restrict__ tv = reinterpret_cast<f32x4*>(th + head);
+    f32x4* __restrict__ mv = reinterpret_cast<f32x4*>(m + head);
+    f32x4* __restrict__ vv = reinterpret_cast<f32x4*>(v + head);
+    u32x2* __restrict__ pv = reinterpret_cast<u32x2*>(p + head);
+    const int64_t b = blockIdx.x;
+
+    // 1. statistics of this workgroup's gradient vectors
+    u32x2 gq[V];
+    double a0 = 0.0, a1 = 0.0;
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+        const int64_t i = (b * V + u) * kSmallBlock + threadIdx.x;
+        gq[u] = i < nvec ? ld<true>(gv + i) : u32x2{0u, 0u};
+        a0 = acc_sq2(gq[u].x, a0);
+        a1 = acc_sq2(gq[u].y, a1);
+    }
+    if (b == 0) {
+        const int64_t t = threadIdx.x;
+        const int64_t tail0 = head + 4 * nvec;
+        if (t < head)
+            a0 += sq1(g[t]);
+        if (t < 4 && tail0 + t < n)
+            a1 += sq1(g[tail0 + t]);
+    }
+    const double ps = block_sum<kSmallBlock>(a0 + a1);
+
+    // 2. publish the partial and arrive; then the state loads
+    if (threadIdx.x == 0) {
+        part[b] = ps;
+        __hip_atomic_fetch_add(bar, (uint64_t)1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    f32x4 tq[V], mq[V], vq[V];
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+        const int64_t i = (b * V + u) * kSmallBlock + threadIdx.x;
+        if (i < nvec) {
+            tq[u] = ld<true>(tv + i);
+            mq[u] = ld<true>(mv + i);
+            vq[u] = ld<true>(vv + i);
+        }
+    }
+
+    // 3. bounded wait for every workgroup's arrival
+    if (threadIdx.x == 0) {
+        uint32_t polls = 0;
+        s_skip = 0;
+        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < bar_target) {
+            __builtin_amdgcn_s_sleep(1);
+            if (++polls >= kBarrierSpinLimit) {
+                s_skip = 2;  // gave up: write nothing
+                break;
+            }
+        }
+    }
+    __syncthreads();
+    if (s_skip == 2)
+        return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other workgroups' partials are visible
+
+    // 4. the total, in the same fixed order in every workgroup
+    double s0 = 0.0;
+    for (int64_t i = threadIdx.x; i < (int64_t)gridDim.x; i += kSmallBlock)
+        s0 += part[i];
+    const double tot = block_sum<kSmallBlock>(s0);
+    if (threadIdx.x == 0) {
+        const Result r = make_result(tot, loss_scale, clip, seq);
+        s_mult = r.mult;
+        s_skip = r.skip;
+        if (b == 0) {
+            *res = r;
+            Result rh = r;
+            rh.seq = 0;
+            *res_host = rh;
+            __hip_atomic_store(&res_host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+    }
+    __syncthreads();
+    if (s_skip)
+        return;
+    const float mult = s_mult;
+
+    // 5. the update from the registers (workgroup 0 also takes head and tail)
+    if (b == 0 && threadIdx.x < 8) {
+        const int64_t t = threadIdx.x;
+        const int64_t i = t < 4 ? t : head + 4 * nvec + (t - 4);
+        if ((t < 4 && i < head) || (t >= 4 && i < n))
+            adam_one(g, th, m, v, p, i, mult, c);
+    }
+#pragma unroll
+    for (int u = 0; u < V; ++u) {
+        const int64_t i = (b * V + u) * kSmallBlock + threadIdx.x;
+        if (i < nvec) {
+            float t[4] = {tq[u].x, tq[u].y, tq[u].z, tq[u].w};
+            float mm[4] = {mq[u].x, mq[u].y, mq[u].z, mq[u].w};
+            float vvv[4] = {vq[u].x, vq[u].y, vq[u].z, vq[u].w};
+            const uint32_t gw[4] = {gq[u].x & 0xFFFFu, gq[u].x >> 16, gq[u].y & 0xFFFFu, gq[u].y >> 16};
+            uint32_t h[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                h[k] = adam_elem(gw[k], mult, t[k], mm[k], vvv[k], c);
+            st<true>(f32x4{t[0], t[1], t[2], t[3]}, tv + i);
+            st<true>(f32x4{mm[0], mm[1], mm[2], mm[3]}, mv + i);
+            st<true>(f32x4{vvv[0], vvv[1], vvv[2], vvv[3]}, vv + i);
+            st<true>(u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)}, pv + i);
+        }
+    }
 }
 
 // Streaming copy of nvec 16-byte vectors: the achievable-bandwidth reference

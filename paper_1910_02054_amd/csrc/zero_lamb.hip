@@ -65,6 +65,7 @@ struct zero_lamb_plan {
     zs::LayerSums* cpart = nullptr;  // one partial per level-1 chunk
     zs::LayerSums* sums = nullptr;   // per-layer sums of zero_lamb_step
     int64_t max_items = 0, max_chunks = 0;
+    hipEvent_t done = nullptr;       // recorded after each call's kernels (ordering across streams)
     hipStream_t last_stream = nullptr;
     bool used = false;
     uint64_t prof_tick = 0;
@@ -82,6 +83,10 @@ zero_lamb_profile_t g_lprof_acc = {0, 0.0, 0.0, 0.0, 0.0};
 template <bool VEC>
 const void* moments_kernel() {
     return reinterpret_cast<const void*>(zs::k_lamb_moments<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, VEC, kLambXCD>);
+}
+template <int PASS>
+const void* probe_kernel() {
+    return reinterpret_cast<const void*>(zs::k_probe_lamb<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, kLambXCD, PASS>);
 }
 template <bool VEC>
 const void* apply_kernel() {
@@ -262,14 +267,20 @@ int check_layer_sums(const char* fn, const zero_lamb_plan_t* plan, const void* l
 }
 
 // Work queued on the plan's previous stream must finish before another
-// stream reuses the plan's partials and sums.  A device-wide wait (rare: only
-// when the stream changes) also covers a previous stream the caller has since
-// destroyed.
+// stream reuses the plan's partials and sums: the new stream waits (on the
+// device) for the event recorded after the plan's last call.  The event stays
+// valid after that stream is destroyed, and no other stream or the host waits.
 int switch_stream(zero_lamb_plan* plan, hipStream_t stream) {
     if (plan->used && plan->last_stream != stream)
-        HIP_TRY(hipDeviceSynchronize());
+        HIP_TRY(hipStreamWaitEvent(stream, plan->done, 0));
     plan->used = true;
     plan->last_stream = stream;
+    return ZERO_OK;
+}
+
+// Marks the end of this call's kernels on `stream` (see switch_stream).
+int mark_done(zero_lamb_plan* plan, hipStream_t stream) {
+    HIP_TRY(hipEventRecord(plan->done, stream));
     return ZERO_OK;
 }
 
@@ -359,12 +370,17 @@ bool lprof_begin(zero_lamb_plan* plan, LambProfRec* rec) {
     return true;
 }
 
-int lprof_drain_locked() {
+void lprof_drain_locked() {
     for (LambProfRec& r : g_lprof_pending) {
-        HIP_TRY(hipEventSynchronize(r.e[4]));
-        float t[4];
-        for (int i = 0; i < 4; ++i)
-            HIP_TRY(hipEventElapsedTime(&t[i], r.e[i], r.e[i + 1]));
+        hipError_t e = hipEventSynchronize(r.e[4]);
+        float t[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < 4 && e == hipSuccess; ++i)
+            e = hipEventElapsedTime(&t[i], r.e[i], r.e[i + 1]);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            prof_defer_error(1, "reading LAMB step events", e);
+            continue;
+        }
         g_lprof_acc.steps += 1;
         g_lprof_acc.stats_ms += t[0];
         g_lprof_acc.moments_ms += t[1];
@@ -375,7 +391,32 @@ int lprof_drain_locked() {
         for (int i = 0; i < 5; ++i)
             g_lprof_pool.push_back(r.e[i]);
     g_lprof_pending.clear();
-    return ZERO_OK;
+}
+
+// Records event i of a sampled step; a failure drops the sample (deferred error).
+void lprof_record(LambProfRec* rec, bool* ok, int i, hipStream_t stream) {
+    if (!*ok)
+        return;
+    const hipError_t e = hipEventRecord(rec->e[i], stream);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *ok = false;
+        prof_defer_error(1, "hipEventRecord", e);
+    }
+}
+
+// Queues a sampled step's record for the next read, or returns its events to
+// the pool when a record failed.
+void lprof_end(const LambProfRec& rec, bool ok) {
+    std::lock_guard<std::mutex> lk(g_lprof_mu);
+    if (!ok) {
+        for (int i = 0; i < 5; ++i)
+            g_lprof_pool.push_back(rec.e[i]);
+        return;
+    }
+    g_lprof_pending.push_back(rec);
+    if (g_lprof_pending.size() >= 4096)
+        lprof_drain_locked();
 }
 
 void set_last_stats(const zs::Result& r, int64_t n) {
@@ -385,9 +426,19 @@ void set_last_stats(const zs::Result& r, int64_t n) {
     t_stats.mult = r.mult;
     t_stats.overflow = r.overflow;
     t_stats.skipped = r.skip;
-    t_stats.pad_ = 0;
+    t_stats.path = 0;
     t_stats.n = n;
     t_have_stats = true;
+}
+
+void free_plan(zero_lamb_plan* p) {
+    for (LambWork& w : p->work)
+        for (void* d : {(void*)w.items, (void*)w.tile_first, (void*)w.chunk, (void*)w.chunk_first})
+            if (d) (void)hipFree(d);
+    if (p->part) (void)hipFree(p->part);
+    if (p->cpart) (void)hipFree(p->cpart);
+    if (p->sums) (void)hipFree(p->sums);
+    if (p->done) (void)hipEventDestroy(p->done);
 }
 
 }  // namespace
@@ -421,19 +472,27 @@ int zero_lamb_plan_create(const int64_t* seg_off, int32_t n_seg, int64_t n, zero
         p->seg_off.assign(1, 0);
     p->max_items = max_items_for(n, n_seg);
     p->max_chunks = max_chunks_for(p->max_items, n_seg);
+    if (hipEventCreateWithFlags(&p->done, hipEventDisableTiming) != hipSuccess) {
+        p->done = nullptr;
+        (void)hipGetLastError();
+        return fail(ZERO_EHIP, "zero_lamb_plan_create: could not create the plan's event");
+    }
     if (n > 0) {
         if (hipMalloc(reinterpret_cast<void**>(&p->part), (size_t)p->max_items * sizeof(zs::LayerSums)) !=
                 hipSuccess ||
             hipMalloc(reinterpret_cast<void**>(&p->cpart), (size_t)p->max_chunks * sizeof(zs::LayerSums)) !=
                 hipSuccess ||
             hipMalloc(reinterpret_cast<void**>(&p->sums), (size_t)n_seg * sizeof(zs::LayerSums)) != hipSuccess) {
-            if (p->part) (void)hipFree(p->part);
-            if (p->cpart) (void)hipFree(p->cpart);
             (void)hipGetLastError();
+            free_plan(p.get());
             return fail(ZERO_ENOMEM, "zero_lamb_plan_create: could not allocate the plan workspace");
         }
         hipDeviceProp_t prop;
-        HIP_TRY(hipGetDeviceProperties(&prop, p->dev));
+        if (hipGetDeviceProperties(&prop, p->dev) != hipSuccess) {
+            (void)hipGetLastError();
+            free_plan(p.get());
+            return fail(ZERO_EHIP, "zero_lamb_plan_create: hipGetDeviceProperties failed");
+        }
         int resident = 0;
         p->lds[0] = occupancy_lds(moments_kernel<true>(), kLambBlock, kLambPerCU, prop, &resident);
         p->lds[1] = occupancy_lds(apply_kernel<true>(), kLambBlock, kLambPerCU, prop, &resident);
@@ -453,14 +512,13 @@ int zero_lamb_plan_destroy(zero_lamb_plan_t* plan) {
         int cur = 0;
         if (hipGetDevice(&cur) == hipSuccess && cur != plan->dev)
             (void)hipSetDevice(plan->dev);
-        if (hipDeviceSynchronize() != hipSuccess)
-            rc = fail(ZERO_EHIP, "zero_lamb_plan_destroy: device synchronisation failed");
-        for (LambWork& w : plan->work)
-            for (void* d : {(void*)w.items, (void*)w.tile_first, (void*)w.chunk, (void*)w.chunk_first})
-                if (d) (void)hipFree(d);
-        if (plan->part) (void)hipFree(plan->part);
-        if (plan->cpart) (void)hipFree(plan->cpart);
-        if (plan->sums) (void)hipFree(plan->sums);
+        // the plan's last call recorded `done` after its kernels, and every call waited
+        // for the previous one's, so this waits for all of the plan's work
+        if (plan->used && hipEventSynchronize(plan->done) != hipSuccess) {
+            (void)hipGetLastError();
+            rc = fail(ZERO_EHIP, "zero_lamb_plan_destroy: waiting for the plan's work failed");
+        }
+        free_plan(plan);
         if (cur != plan->dev)
             (void)hipSetDevice(cur);
     }
@@ -489,45 +547,39 @@ int zero_lamb_step(const zero_lamb_plan_t* plan_, const uint16_t* grad16, float*
         return ZERO_OK;
     }
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
-        return rc;
     std::lock_guard<std::mutex> plk(plan->mu);
-    std::lock_guard<std::mutex> lk(ctx->mu);
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
+        return rc;
     const int phase = phase_of(grad16, master32, m32, v32, param16_out);
     LambWork* w = nullptr;
     if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
-    const uint32_t seq = next_seq(ctx);
+    const uint32_t seq = next_seq(ctx.get());
     LambProfRec pr;
-    const bool prof = lprof_begin(plan, &pr);
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[0], stream));
-    if ((rc = launch_stats_planned(ctx, grad16, n, loss_scale, clip, seq, stream)))
+    bool prof = lprof_begin(plan, &pr);
+    const bool sampled = prof;
+    lprof_record(&pr, &prof, 0, stream);
+    rc = launch_stats_planned(ctx.get(), grad16, n, loss_scale, clip, seq, stream);
+    lprof_record(&pr, &prof, 1, stream);
+    if (!rc)
+        rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream);
+    lprof_record(&pr, &prof, 2, stream);
+    if (!rc)
+        rc = launch_layer(plan, *w, plan->sums, ctx->res, stream);
+    lprof_record(&pr, &prof, 3, stream);
+    if (!rc)
+        rc = launch_apply(plan, *w, phase, master32, m32, v32, param16_out, plan->sums, ctx->res, c, lr, phi_lo,
+                          phi_hi, stream);
+    lprof_record(&pr, &prof, 4, stream);
+    if (sampled)
+        lprof_end(pr, prof && !rc);
+    const int rc_done = mark_done(plan, stream);
+    if (rc || (rc = rc_done))
         return rc;
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[1], stream));
-    if ((rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream)))
-        return rc;
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[2], stream));
-    if ((rc = launch_layer(plan, *w, plan->sums, ctx->res, stream)))
-        return rc;
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.e[3], stream));
-    if ((rc = launch_apply(plan, *w, phase, master32, m32, v32, param16_out, plan->sums, ctx->res, c, lr, phi_lo,
-                           phi_hi, stream)))
-        return rc;
-    if (prof) {
-        HIP_TRY(hipEventRecord(pr.e[4], stream));
-        std::lock_guard<std::mutex> lk2(g_lprof_mu);
-        g_lprof_pending.push_back(pr);
-        if (g_lprof_pending.size() >= 4096 && (rc = lprof_drain_locked()))
-            return rc;
-    }
     zs::Result r;
-    if ((rc = wait_result(ctx, seq, stream, &r)))
+    if ((rc = wait_result(ctx.get(), seq, stream, &r)))
         return rc;
     set_last_stats(r, n);
     return r.skip ? ZERO_SKIPPED : ZERO_OK;
@@ -556,22 +608,24 @@ int zero_lamb_moments(const zero_lamb_plan_t* plan_, const uint16_t* grad16, con
     if (n == 0)
         return ZERO_OK;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
-        return rc;
     std::lock_guard<std::mutex> plk(plan->mu);
-    std::lock_guard<std::mutex> lk(ctx->mu);
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
+        return rc;
     const int phase = phase_of(grad16, master32, m32, v32, nullptr);
     LambWork* w = nullptr;
     if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
         return rc;
     const zs::AdamConst c = adam_const(0.0, beta1, beta2, eps, weight_decay, step);
-    const uint32_t seq = next_seq(ctx);
+    const uint32_t seq = next_seq(ctx.get());
     zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
-    HIP_TRY(hipGetLastError());
-    if ((rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream)))
-        return rc;
-    return launch_layer(plan, *w, reinterpret_cast<zs::LayerSums*>(layer_sumsq), ctx->res, stream);
+    rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "%s: result-record launch failed", fn);
+    if (!rc)
+        rc = launch_moments(plan, *w, phase, grad16, master32, m32, v32, ctx->res, c, stream);
+    if (!rc)
+        rc = launch_layer(plan, *w, reinterpret_cast<zs::LayerSums*>(layer_sumsq), ctx->res, stream);
+    const int rc_done = mark_done(plan, stream);
+    return rc ? rc : rc_done;
 }
 
 int zero_lamb_apply(const zero_lamb_plan_t* plan_, float* master32, const float* m32, const float* v32,
@@ -599,34 +653,75 @@ int zero_lamb_apply(const zero_lamb_plan_t* plan_, float* master32, const float*
     if (n == 0)
         return ZERO_OK;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
-        return rc;
     std::lock_guard<std::mutex> plk(plan->mu);
-    std::lock_guard<std::mutex> lk(ctx->mu);
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
+        return rc;
     const int phase = phase_of(nullptr, master32, m32, v32, param16_out);
     LambWork* w = nullptr;
     if ((rc = get_work(plan, phase, &w)) || (rc = switch_stream(plan, stream)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
-    const uint32_t seq = next_seq(ctx);
+    const uint32_t seq = next_seq(ctx.get());
     // the apply kernel reads only the skip flag of the record: not skipped here
     zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, 0.0, 1.0, 0.0, seq);
+    rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "%s: result-record launch failed", fn);
+    if (!rc)
+        rc = launch_apply(plan, *w, phase, master32, m32, v32, param16_out,
+                          reinterpret_cast<const zs::LayerSums*>(layer_sumsq), ctx->res, c, lr, phi_lo, phi_hi,
+                          stream);
+    const int rc_done = mark_done(plan, stream);
+    return rc ? rc : rc_done;
+}
+
+int zero_probe_lamb_pass(int32_t pass, const uint16_t* grad16, float* master32, float* m32, float* v32,
+                         uint16_t* param16_out, int64_t n, void* stream_) {
+    const char* fn = "zero_probe_lamb_pass";
+    if (pass != 0 && pass != 1)
+        return fail(ZERO_EINVAL, "%s: pass must be 0 (moments) or 1 (apply)", fn);
+    if (n < 0 || n > kMaxNumel)
+        return fail(ZERO_EINVAL, "%s: n=%lld outside [0, 2^40]", fn, (long long)n);
+    if (n == 0)
+        return ZERO_OK;
+    const void* arrays[5] = {pass == 0 ? grad16 : nullptr, master32, m32, v32, pass == 1 ? param16_out : nullptr};
+    static const size_t align[5] = {8, 16, 16, 16, 8};
+    for (int i = 0; i < 5; ++i)
+        if (arrays[i] == nullptr && ((pass == 0 && i != 4) || (pass == 1 && i != 0)))
+            return fail(ZERO_EINVAL, "%s: NULL array %d", fn, i);
+        else if (arrays[i] && reinterpret_cast<uintptr_t>(arrays[i]) % align[i])
+            return fail(ZERO_EINVAL, "%s: array %d must be %zu-byte aligned", fn, i, align[i]);
+    int rc = check_lamb_arrays(fn, arrays, n);
+    if (rc)
+        return rc;
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    hipDeviceProp_t prop;
+    HIP_TRY(hipGetDeviceProperties(&prop, dev));
+    const void* kern = pass == 0 ? probe_kernel<0>() : probe_kernel<1>();
+    int resident = 0;
+    const size_t lds = occupancy_lds(kern, kLambBlock, kLambPerCU, prop, &resident);
+    const int64_t ntiles = (n + kLambTile - 1) / kLambTile;
+    const unsigned grid = tile_grid(ntiles);
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    if (pass == 0)
+        zs::k_probe_lamb<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, kLambXCD, 0>
+            <<<grid, kLambBlock, lds, stream>>>(grad16, master32, m32, v32, param16_out, ntiles, n);
+    else
+        zs::k_probe_lamb<kLambBlock, kLambUnroll, kLambNTL, kLambNTS, kLambXCD, 1>
+            <<<grid, kLambBlock, lds, stream>>>(grad16, master32, m32, v32, param16_out, ntiles, n);
     HIP_TRY(hipGetLastError());
-    return launch_apply(plan, *w, phase, master32, m32, v32, param16_out,
-                        reinterpret_cast<const zs::LayerSums*>(layer_sumsq), ctx->res, c, lr, phi_lo, phi_hi, stream);
+    return ZERO_OK;
 }
 
 int zero_lamb_profile_read(zero_lamb_profile_t* out) {
     if (!out)
         return fail(ZERO_EINVAL, "zero_lamb_profile_read: NULL out");
     std::lock_guard<std::mutex> lk(g_lprof_mu);
-    int rc = lprof_drain_locked();
-    if (rc)
-        return rc;
+    lprof_drain_locked();
+    const int rc = prof_take_error(1);
     *out = g_lprof_acc;
     g_lprof_acc = zero_lamb_profile_t{0, 0.0, 0.0, 0.0, 0.0};
-    return ZERO_OK;
+    return rc;
 }
 
 }  // extern "C"

@@ -13,6 +13,7 @@
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <map>
 #include <memory>
@@ -58,6 +59,19 @@ constexpr bool kAdamNTL = true, kAdamNTS = true, kAdamXCD = false, kAdamREV = fa
 constexpr int64_t kAdamMaxBlocks = 1 << 26;
 constexpr int kCopyBlock = 64, kCopyUnroll = 1;
 constexpr bool kCopyNTL = true, kCopyNTS = true, kCopyXCD = false;
+// One-launch small-shard step (k_small_step): shards of at most kSmallMaxNumel
+// elements whose arrays share one misalignment, on a grid of at most
+// kSmallMaxGrid workgroups (each totals every workgroup's partial).
+#ifndef ZS_SMALL_MAX_NUMEL
+#define ZS_SMALL_MAX_NUMEL (1 << 22)
+#endif
+constexpr int64_t kSmallMaxNumel = ZS_SMALL_MAX_NUMEL;
+constexpr int64_t kSmallMaxGrid = 512;
+// A grid takes at most 1/kSmallCapShare of the device's co-resident capacity,
+// so the barrier-waiting workgroups of cooperative steps running at once on
+// several streams (the hardware queues a process gets) always fit together.
+constexpr int64_t kSmallCapShare = 8;
+constexpr int kSmallV[4] = {1, 2, 4, 8};
 
 // ---------------------------------------------------------------------------
 // Launch planning.  One function decides every launch shape from n and the
@@ -69,6 +83,8 @@ struct Plan {
     bool vec;              // update: vector path (all arrays share misalignment)
     int64_t head, nvec;    // update: head elements, 4-element vectors
     int64_t adam_blocks;
+    int small_v;           // one-launch small-shard step: vectors per thread (0: not taken)
+    int64_t small_grid;
 };
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -105,6 +121,26 @@ Plan plan_step(const uint16_t* g, const float* th, const float* m, const float* 
     return pl;
 }
 
+// The one-launch small-shard step when the shard qualifies: the fewest vectors
+// per thread whose grid fits both kSmallMaxGrid and the device's co-resident
+// capacity for that kernel.
+void plan_small(Plan* pl, int64_t n, const DevInfo* info) {
+    pl->small_v = 0;
+    pl->small_grid = 0;
+    if (!pl->vec || n > kSmallMaxNumel)
+        return;
+    for (int k = 0; k < 4; ++k) {
+        int64_t grid = ceil_div(pl->nvec, (int64_t)zs::kSmallBlock * kSmallV[k]);
+        if (grid < 1)
+            grid = 1;
+        if (grid <= kSmallMaxGrid && grid <= info->small_cap[k] / kSmallCapShare) {
+            pl->small_v = kSmallV[k];
+            pl->small_grid = grid;
+            return;
+        }
+    }
+}
+
 // Dynamic LDS that caps the resident workgroups of `kernel` (launched with
 // `block` threads) at `per_cu` per CU: an equal share of the CU's LDS minus the
 // kernel's own static LDS, lowered granule by granule until the runtime's
@@ -137,76 +173,202 @@ size_t occupancy_lds(const void* kernel, int block, int per_cu, const hipDeviceP
     }
 }
 
+const void* small_kernel(int v) {
+    switch (v) {
+    case 1: return reinterpret_cast<const void*>(zs::k_small_step<1>);
+    case 2: return reinterpret_cast<const void*>(zs::k_small_step<2>);
+    case 4: return reinterpret_cast<const void*>(zs::k_small_step<4>);
+    default: return reinterpret_cast<const void*>(zs::k_small_step<8>);
+    }
+}
+
 // ---------------------------------------------------------------------------
-// Per-(device, stream) context (struct Ctx in host_common.hpp).
+// Per-device facts, computed once per device into a fixed table.
+// ---------------------------------------------------------------------------
+std::mutex g_dev_mu;
+DevInfo g_dev[kMaxDevices];
+std::atomic<bool> g_dev_ready[kMaxDevices];
+
+int dev_info(int dev, const DevInfo** out) {
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(ZERO_EINVAL, "device %d is outside the library's table of %d devices", dev, kMaxDevices);
+    if (!g_dev_ready[dev].load(std::memory_order_acquire)) {
+        std::lock_guard<std::mutex> lk(g_dev_mu);
+        if (!g_dev_ready[dev].load(std::memory_order_relaxed)) {
+            hipDeviceProp_t prop;
+            HIP_TRY(hipGetDeviceProperties(&prop, dev));
+            DevInfo d;
+            d.ncu = prop.multiProcessorCount;
+            d.stats_lds = occupancy_lds(
+                reinterpret_cast<const void*>(zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>),
+                kStatsBlock, kStatsPerCU, prop, &d.stats_resident);
+            d.adam_lds = occupancy_lds(
+                reinterpret_cast<const void*>(
+                    zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>),
+                kAdamBlock, kAdamPerCU, prop, &d.adam_resident);
+            int coop = 0;
+            if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) {
+                (void)hipGetLastError();
+                coop = 0;
+            }
+            for (int k = 0; k < 4 && coop; ++k) {
+                int per_cu = 0;
+                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, small_kernel(kSmallV[k]), zs::kSmallBlock,
+                                                                 0) != hipSuccess) {
+                    (void)hipGetLastError();
+                    per_cu = 0;
+                }
+                d.small_cap[k] = (int64_t)per_cu * d.ncu;
+            }
+            g_dev[dev] = d;
+            g_dev_ready[dev].store(true, std::memory_order_release);
+        }
+    }
+    *out = &g_dev[dev];
+    return ZERO_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Per-(device, stream) contexts (struct Ctx in host_common.hpp).
 // ---------------------------------------------------------------------------
 
 std::mutex g_ctx_mu;
-std::map<std::pair<int, hipStream_t>, std::unique_ptr<Ctx>> g_ctx;
+std::map<std::pair<int, hipStream_t>, std::shared_ptr<Ctx>> g_ctx;
 
-int get_ctx(hipStream_t stream, Ctx** out) {
-    int dev = 0;
-    HIP_TRY(hipGetDevice(&dev));
-    if (stream) {
-        hipDevice_t sdev = 0;
-        HIP_TRY(hipStreamGetDevice(stream, &sdev));
-        if ((int)sdev != dev)
-            return fail(ZERO_EINVAL, "stream belongs to device %d but the current device is %d", (int)sdev, dev);
+void free_ctx_buffers(Ctx* c) {
+    if (c->part) (void)hipFree(c->part);
+    if (c->res) (void)hipFree(c->res);
+    if (c->bar) (void)hipFree(c->bar);
+    if (c->host) (void)hipHostFree(c->host);
+    c->part = nullptr;
+    c->res = nullptr;
+    c->bar = nullptr;
+    c->host = c->host_dev = nullptr;
+}
+
+// Allocations made while `stream` may be capturing a graph switch this thread
+// to the relaxed capture mode, in which allocating is permitted.
+struct RelaxedCapture {
+    bool on = false;
+    hipStreamCaptureMode mode = hipStreamCaptureModeRelaxed;
+    explicit RelaxedCapture(hipStream_t stream) {
+        hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+            (void)hipGetLastError();
+            return;
+        }
+        if (st != hipStreamCaptureStatusNone && hipThreadExchangeStreamCaptureMode(&mode) == hipSuccess)
+            on = true;
     }
-    std::lock_guard<std::mutex> lk(g_ctx_mu);
-    auto key = std::make_pair(dev, stream);
-    auto it = g_ctx.find(key);
-    if (it != g_ctx.end()) {
-        *out = it->second.get();
-        return 0;
+    ~RelaxedCapture() {
+        if (on)
+            (void)hipThreadExchangeStreamCaptureMode(&mode);
     }
-    hipDeviceProp_t prop;
-    HIP_TRY(hipGetDeviceProperties(&prop, dev));
-    std::unique_ptr<Ctx> c(new Ctx);
-    c->ncu = prop.multiProcessorCount;
-    c->stats_lds = occupancy_lds(
-        reinterpret_cast<const void*>(zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>), kStatsBlock,
-        kStatsPerCU, prop, &c->stats_resident);
-    c->adam_lds = occupancy_lds(
-        reinterpret_cast<const void*>(
-            zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>),
-        kAdamBlock, kAdamPerCU, prop, &c->adam_resident);
+};
+
+int new_ctx(int dev, hipStream_t stream, const DevInfo* info, std::shared_ptr<Ctx>* out) {
+    std::shared_ptr<Ctx> c = std::make_shared<Ctx>();
+    c->dev = dev;
+    c->stream = stream;
+    c->info = info;
+    RelaxedCapture relaxed(stream);
+    // the barrier counter is zeroed on the stream before the first small-shard launch
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
-              hipMalloc(reinterpret_cast<void**>(&c->dconst), sizeof(zs::AdamConst)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->bar), sizeof(uint64_t)) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
               hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess;
     if (!ok) {
-        if (c->part) (void)hipFree(c->part);
-        if (c->res) (void)hipFree(c->res);
-        if (c->dconst) (void)hipFree(c->dconst);
-        if (c->host) (void)hipHostFree(c->host);
+        free_ctx_buffers(c.get());
         (void)hipGetLastError();
         return fail(ZERO_ENOMEM, "could not allocate the step workspace on device %d", dev);
     }
     std::memset(c->host, 0, sizeof(zs::Result));
-    *out = c.get();
-    g_ctx.emplace(key, std::move(c));
-    return 0;
+    *out = std::move(c);
+    return ZERO_OK;
+}
+
+// The device of the calling thread, and a check that `stream` belongs to it.
+int current_device(hipStream_t stream, int* dev) {
+    HIP_TRY(hipGetDevice(dev));
+    if (stream) {
+        hipDevice_t sdev = 0;
+        HIP_TRY(hipStreamGetDevice(stream, &sdev));
+        if ((int)sdev != *dev)
+            return fail(ZERO_EINVAL, "stream belongs to device %d but the current device is %d", (int)sdev, *dev);
+    }
+    return ZERO_OK;
+}
+
+int lock_ctx(hipStream_t stream, CtxLock* out) {
+    int dev = 0;
+    int rc = current_device(stream, &dev);
+    const DevInfo* info = nullptr;
+    if (rc || (rc = dev_info(dev, &info)))
+        return rc;
+    const auto key = std::make_pair(dev, stream);
+    for (;;) {
+        std::shared_ptr<Ctx> c;
+        {
+            std::lock_guard<std::mutex> lk(g_ctx_mu);
+            auto it = g_ctx.find(key);
+            if (it != g_ctx.end()) {
+                c = it->second;
+            } else {
+                if ((rc = new_ctx(dev, stream, info, &c)))
+                    return rc;
+                g_ctx.emplace(key, c);
+            }
+        }
+        std::unique_lock<std::mutex> lk(c->mu);
+        if (c->released)
+            continue;  // released since the lookup: the registry holds a fresh one (or none)
+        out->ref = std::move(c);
+        out->lk = std::move(lk);
+        return ZERO_OK;
+    }
 }
 
 // ---------------------------------------------------------------------------
-// Profiling: two events per step, before and after the update kernel.  The
-// statistics time of a step runs from the previous profiled update's end on
-// the same stream (or from an extra start event for the first one) to the
-// update's start.
+// Profiling: three events per sampled step (before the statistics, before the
+// update, after it), each step with its own events.  Failures after a step's
+// kernels are queued are deferred to the read call.
 // ---------------------------------------------------------------------------
 struct ProfRec {
     hipEvent_t start, mid, end;
-    bool own_start;  // start was recorded for this step (else it is the previous step's end)
+    bool ok;
 };
 
 std::mutex g_prof_mu;
 int32_t g_prof_every = 0;  // 0: off; k: profile one step in k on each stream
+uint64_t g_prof_epoch = 1;
 std::vector<ProfRec> g_prof_pending;
 std::vector<hipEvent_t> g_prof_pool;
 zero_profile_t g_prof_acc = {0, 0.0, 0.0};
+
+std::mutex g_prof_err_mu;
+std::string g_prof_err[2];
+int g_prof_err_code[2] = {0, 0};
+
+void prof_defer_error(int slot, const char* what, hipError_t e) {
+    std::lock_guard<std::mutex> lk(g_prof_err_mu);
+    if (g_prof_err_code[slot] == 0) {  // keep the first
+        g_prof_err_code[slot] = ZERO_EHIP;
+        g_prof_err[slot] = std::string("profiling: ") + what + ": " + hipGetErrorString(e);
+    }
+}
+
+int prof_take_error(int slot) {
+    std::lock_guard<std::mutex> lk(g_prof_err_mu);
+    const int code = g_prof_err_code[slot];
+    if (code) {
+        t_err = g_prof_err[slot];
+        g_prof_err_code[slot] = 0;
+        g_prof_err[slot].clear();
+    }
+    return code;
+}
 
 hipEvent_t prof_event() {
     if (!g_prof_pool.empty()) {
@@ -215,37 +377,86 @@ hipEvent_t prof_event() {
         return e;
     }
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess)
+    if (hipEventCreate(&e) != hipSuccess) {
+        (void)hipGetLastError();
         return nullptr;
+    }
     return e;
 }
 
-// Forget every stream's last end event (its handle is about to go back to the pool).
-void prof_forget_ends() {
-    std::lock_guard<std::mutex> lk(g_ctx_mu);
-    for (auto& kv : g_ctx)
-        kv.second->prof_last_end = nullptr;
-}
-
-int prof_drain_locked() {
+// Sums the pending records into the totals and returns their events to the
+// pool; a failed query is deferred and the record dropped.
+void prof_drain_locked() {
     for (ProfRec& r : g_prof_pending) {
-        HIP_TRY(hipEventSynchronize(r.end));
+        hipError_t e = hipEventSynchronize(r.end);
         float a = 0.f, b = 0.f;
-        HIP_TRY(hipEventElapsedTime(&a, r.start, r.mid));
-        HIP_TRY(hipEventElapsedTime(&b, r.mid, r.end));
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&a, r.start, r.mid);
+        if (e == hipSuccess)
+            e = hipEventElapsedTime(&b, r.mid, r.end);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            prof_defer_error(0, "reading step events", e);
+            continue;
+        }
         g_prof_acc.steps += 1;
         g_prof_acc.stats_ms += a;
         g_prof_acc.update_ms += b;
     }
     for (ProfRec& r : g_prof_pending) {
-        if (r.own_start)
-            g_prof_pool.push_back(r.start);
+        g_prof_pool.push_back(r.start);
         g_prof_pool.push_back(r.mid);
         g_prof_pool.push_back(r.end);
     }
     g_prof_pending.clear();
-    prof_forget_ends();
-    return 0;
+}
+
+// 1 when this step is sampled (rec holds three events), 0 when not, or an
+// error (nothing queued yet) when the events cannot be had.
+int prof_begin(uint64_t* tick, uint64_t* epoch, ProfRec* rec) {
+    std::lock_guard<std::mutex> plk(g_prof_mu);
+    if (g_prof_every <= 0)
+        return 0;
+    if (*epoch != g_prof_epoch) {
+        *epoch = g_prof_epoch;
+        *tick = 0;
+    }
+    if ((*tick)++ % (uint64_t)g_prof_every != 0)
+        return 0;
+    rec->start = prof_event();
+    rec->mid = prof_event();
+    rec->end = prof_event();
+    rec->ok = rec->start && rec->mid && rec->end;
+    if (!rec->ok) {
+        for (hipEvent_t e : {rec->start, rec->mid, rec->end})
+            if (e)
+                g_prof_pool.push_back(e);
+        return fail(ZERO_EHIP, "could not create a profiling event");
+    }
+    return 1;
+}
+
+void prof_record(hipEvent_t e, hipStream_t stream, ProfRec* rec) {
+    if (!rec->ok)
+        return;
+    const hipError_t r = hipEventRecord(e, stream);
+    if (r != hipSuccess) {
+        (void)hipGetLastError();
+        rec->ok = false;
+        prof_defer_error(0, "hipEventRecord", r);
+    }
+}
+
+void prof_end(const ProfRec& rec) {
+    std::lock_guard<std::mutex> plk(g_prof_mu);
+    if (!rec.ok) {
+        for (hipEvent_t e : {rec.start, rec.mid, rec.end})
+            g_prof_pool.push_back(e);
+        return;
+    }
+    g_prof_pending.push_back(rec);
+    if (g_prof_pending.size() >= 4096)
+        prof_drain_locked();
 }
 
 bool is_fin(double x) { return std::isfinite(x); }
@@ -307,6 +518,8 @@ int check_arrays(const char* fn, const uint16_t* grad16, const float* master32, 
 
 int check_hyper(const char* fn, double lr, double beta1, double beta2, double eps, double weight_decay, int64_t step,
                 double loss_scale, double clip) {
+    if (zs::hyper_ok(lr, beta1, beta2, eps, weight_decay, step, loss_scale, clip))
+        return ZERO_OK;
     if (!is_fin(lr) || lr < 0.0 || !is_fin(eps) || eps < 0.0 || !is_fin(weight_decay))
         return fail(ZERO_EINVAL, "%s: need finite lr >= 0, eps >= 0, weight_decay", fn);
     if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
@@ -315,9 +528,7 @@ int check_hyper(const char* fn, double lr, double beta1, double beta2, double ep
         return fail(ZERO_EINVAL, "%s: step (t) must be >= 1, got %lld", fn, (long long)step);
     if (!is_fin(loss_scale) || !(loss_scale > 0.0))
         return fail(ZERO_EINVAL, "%s: loss_scale must be finite and > 0", fn);
-    if (std::isnan(clip))
-        return fail(ZERO_EINVAL, "%s: clip is NaN", fn);
-    return ZERO_OK;
+    return fail(ZERO_EINVAL, "%s: clip is NaN", fn);
 }
 
 int check_update_args(const char* fn, const uint16_t* grad16, const float* master32, const float* m32,
@@ -356,38 +567,29 @@ int check_shard_ranges(const char* fn, const uint16_t* grad16, const float* mast
     return check_ranges(fn, ptrs, bytes, 5);
 }
 
-// fp32 constants, each computed in double and rounded once (the bias
-// corrections 1 - beta^t use the C library's pow).
+// fp32 constants, each computed in double and rounded once; the bias
+// corrections come from the definition the resident step's kernel shares.
 zs::AdamConst adam_const(double lr, double beta1, double beta2, double eps, double wd, int64_t step) {
-    zs::AdamConst c;
-    c.lr = (float)lr;
-    c.b1 = (float)beta1;
-    c.omb1 = (float)(1.0 - beta1);
-    c.b2 = (float)beta2;
-    c.omb2 = (float)(1.0 - beta2);
-    c.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
-    c.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
-    c.eps = (float)eps;
-    c.wd = (float)wd;
-    return c;
+    return zs::make_adam_const(lr, beta1, beta2, eps, wd, step);
 }
 
-// Statistics + finalize: the result record lands in ctx->res and ctx->host.
-int launch_stats(Ctx* ctx, const uint16_t* grad16, int64_t n, const Plan& pl, double loss_scale, double clip,
-                 uint32_t seq, hipStream_t stream) {
+// Statistics + finalize: the result record lands in res and host_dev.
+int launch_stats_into(const DevInfo* info, zs::Partial* part, zs::Result* res, zs::Result* host_dev,
+                      const uint16_t* grad16, int64_t n, const Plan& pl, double loss_scale, double clip, uint32_t seq,
+                      hipStream_t stream) {
     zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
-        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+        <<<pl.stats_blocks, kStatsBlock, info->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, part);
     HIP_TRY(hipGetLastError());
-    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, ctx->res, ctx->host_dev,
-                                                      loss_scale, clip, seq);
+    zs::k_finalize<<<1, zs::kFinalBlock, 0, stream>>>(part, pl.stats_blocks, res, host_dev, loss_scale, clip, seq);
     HIP_TRY(hipGetLastError());
     return ZERO_OK;
 }
 
 int launch_stats_planned(Ctx* ctx, const uint16_t* grad16, int64_t n, double loss_scale, double clip, uint32_t seq,
                          hipStream_t stream) {
-    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
-    return launch_stats(ctx, grad16, n, pl, loss_scale, clip, seq, stream);
+    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->info->ncu);
+    return launch_stats_into(ctx->info, ctx->part, ctx->res, ctx->host_dev, grad16, n, pl, loss_scale, clip, seq,
+                             stream);
 }
 
 int prof_every() {
@@ -395,26 +597,60 @@ int prof_every() {
     return g_prof_every;
 }
 
-// The fused update reading its scalars from ctx->res; the fp32 constants are
+// The fused update reading its scalars from `res`; the fp32 constants are
 // `c`, or the device copy at cdev when it is not NULL.
-int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
-                  int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream,
-                  const zs::AdamConst* cdev = nullptr) {
+int launch_update_from(const DevInfo* info, const zs::Result* res, const uint16_t* grad16, float* master32,
+                       float* m32, float* v32, uint16_t* param16_out, int64_t n, const Plan& pl,
+                       const zs::AdamConst& c, hipStream_t stream, const zs::AdamConst* cdev = nullptr) {
     if (pl.vec && cdev)
         zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, true>
-            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
-                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c, cdev);
+            <<<(unsigned)pl.adam_blocks, kAdamBlock, info->adam_lds, stream>>>(
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, res, c, cdev);
     else if (pl.vec)
         zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>
-            <<<(unsigned)pl.adam_blocks, kAdamBlock, ctx->adam_lds, stream>>>(
-                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, ctx->res, c, nullptr);
+            <<<(unsigned)pl.adam_blocks, kAdamBlock, info->adam_lds, stream>>>(
+                grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, res, c, nullptr);
     else if (cdev)
         zs::k_adam_scalar<true><<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
-            grad16, master32, m32, v32, param16_out, n, ctx->res, c, cdev);
+            grad16, master32, m32, v32, param16_out, n, res, c, cdev);
     else
         zs::k_adam_scalar<false><<<(unsigned)pl.adam_blocks, zs::kScalarBlock, 0, stream>>>(
-            grad16, master32, m32, v32, param16_out, n, ctx->res, c, nullptr);
+            grad16, master32, m32, v32, param16_out, n, res, c, nullptr);
     HIP_TRY(hipGetLastError());
+    return ZERO_OK;
+}
+
+int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                  int64_t n, const Plan& pl, const zs::AdamConst& c, hipStream_t stream) {
+    return launch_update_from(ctx->info, ctx->res, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
+}
+
+// The one-launch small-shard step (pl.small_v > 0) with its partials in `part`
+// and its barrier counter at `bar`, whose arrivals so far are *bar_count
+// (advanced by the grid when the launch is accepted).
+int launch_small_into(double* part, uint64_t* bar, uint64_t* bar_count, bool* bar_ready, zs::Result* res,
+                      zs::Result* host_dev, const uint16_t* grad16, float* master32, float* m32, float* v32,
+                      uint16_t* param16_out, int64_t n, const Plan& pl, double loss_scale, double clip, uint32_t seq,
+                      const zs::AdamConst& c, hipStream_t stream) {
+    if (!*bar_ready) {
+        zs::k_set_u64<<<1, 64, 0, stream>>>(bar, 0);
+        HIP_TRY(hipGetLastError());
+        *bar_count = 0;
+        *bar_ready = true;
+    }
+    const uint64_t target = *bar_count + (uint64_t)pl.small_grid;
+    int64_t head = pl.head, nvec = pl.nvec;
+    void* args[] = {&grad16, &master32, &m32, &v32, &param16_out, &n, &head, &nvec, &part, &bar,
+                    const_cast<uint64_t*>(&target), &res, &host_dev, &loss_scale, &clip, &seq,
+                    const_cast<zs::AdamConst*>(&c)};
+    const hipError_t e = hipLaunchCooperativeKernel(small_kernel(pl.small_v), dim3((unsigned)pl.small_grid),
+                                                    dim3(zs::kSmallBlock), args, 0, stream);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ZERO_EHIP, "cooperative launch of the small-shard step (%lld workgroups): %s",
+                    (long long)pl.small_grid, hipGetErrorString(e));
+    }
+    *bar_count = target;
     return ZERO_OK;
 }
 
@@ -447,40 +683,65 @@ int wait_result(Ctx* ctx, uint32_t seq, hipStream_t stream, zs::Result* out) {
     return ZERO_OK;
 }
 
-// Profiling events of one step (taken from a pool while profiling is on).
-// Returns false when profiling is off; rec->end == nullptr signals failure.
-// With chain, a step that directly follows a profiled step on the stream takes
-// that step's end event as its start.
-bool prof_begin(Ctx* ctx, ProfRec* rec, bool chain = true) {
-    std::lock_guard<std::mutex> plk(g_prof_mu);
-    if (g_prof_every <= 0)
-        return false;
-    if (ctx->prof_tick++ % (uint64_t)g_prof_every != 0) {
-        ctx->prof_last_end = nullptr;  // the chain of back-to-back profiled steps is broken
-        return false;
-    }
-    rec->own_start = !chain || ctx->prof_last_end == nullptr;
-    rec->start = rec->own_start ? prof_event() : ctx->prof_last_end;
-    rec->mid = prof_event();
-    rec->end = prof_event();
-    if (!rec->start || !rec->mid || !rec->end) {
-        if (rec->own_start && rec->start)
-            g_prof_pool.push_back(rec->start);
-        if (rec->mid)
-            g_prof_pool.push_back(rec->mid);
-        if (rec->end)
-            g_prof_pool.push_back(rec->end);
-        rec->end = nullptr;
-    }
-    return true;
+void set_stats(const zs::Result& r, int64_t n, int32_t path) {
+    t_stats.sumsq = r.sumsq;
+    t_stats.norm = r.norm;
+    t_stats.coef = r.coef;
+    t_stats.mult = r.mult;
+    t_stats.overflow = r.overflow;
+    t_stats.skipped = r.skip;
+    t_stats.path = path;
+    t_stats.n = n;
+    t_have_stats = true;
 }
 
-int prof_end(Ctx* ctx, const ProfRec& rec) {
-    std::lock_guard<std::mutex> plk(g_prof_mu);
-    g_prof_pending.push_back(rec);
-    ctx->prof_last_end = rec.end;
-    if (g_prof_pending.size() >= 4096)
-        return prof_drain_locked();
+// ---------------------------------------------------------------------------
+// Resident-step workspaces, one per (device, state record): every step taken
+// with a record, eager or replayed from a captured graph, uses that record's
+// workspace, so steps with different records never share one.
+// ---------------------------------------------------------------------------
+struct ResWs {
+    zs::Partial* part = nullptr;
+    zs::Result* res = nullptr;
+    zs::AdamConst* dconst = nullptr;
+    uint32_t seq = 0;          // call counter echoed in the result record
+    uint64_t prof_tick = 0;    // sampled timing, as a stream context's
+    uint64_t prof_epoch = 0;
+};
+
+std::mutex g_res_mu;
+std::map<std::pair<int, const void*>, ResWs> g_res;  // node addresses stay valid until erased
+
+void free_res_ws(ResWs* w) {
+    if (w->part) (void)hipFree(w->part);
+    if (w->res) (void)hipFree(w->res);
+    if (w->dconst) (void)hipFree(w->dconst);
+    *w = ResWs{};
+}
+
+// The workspace of `state` on device `dev`, allocated on first use (also while
+// `stream` is capturing).  Steps with one record do not overlap, so the caller
+// may use the entry without holding the lock.
+int resident_ws(int dev, const void* state, hipStream_t stream, ResWs** out) {
+    std::lock_guard<std::mutex> lk(g_res_mu);
+    const auto key = std::make_pair(dev, state);
+    auto it = g_res.find(key);
+    if (it != g_res.end()) {
+        *out = &it->second;
+        return ZERO_OK;
+    }
+    RelaxedCapture relaxed(stream);
+    ResWs w;
+    const bool ok = hipMalloc(reinterpret_cast<void**>(&w.part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) ==
+                        hipSuccess &&
+                    hipMalloc(reinterpret_cast<void**>(&w.res), sizeof(zs::Result)) == hipSuccess &&
+                    hipMalloc(reinterpret_cast<void**>(&w.dconst), sizeof(zs::AdamConst)) == hipSuccess;
+    if (!ok) {
+        free_res_ws(&w);
+        (void)hipGetLastError();
+        return fail(ZERO_ENOMEM, "could not allocate the resident step's workspace on device %d", dev);
+    }
+    *out = &g_res.emplace(key, w).first->second;
     return ZERO_OK;
 }
 
@@ -514,7 +775,7 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
 }
 
 int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, double* out) {
-    if (!out || !(nd > 0.0) || !(psi >= 0.0) || !is_fin(k))
+    if (!out || !(nd > 0.0) || !is_fin(nd) || !(psi >= 0.0) || !is_fin(psi) || !is_fin(k))
         return fail(ZERO_EINVAL, "zero_model_state_bytes: invalid psi/nd/k or NULL out");
     // fp16 parameters and gradients take 2 bytes each, the optimizer state K bytes per parameter.
     const double params = 2.0 * psi, grads = 2.0 * psi, opt = k * psi;
@@ -525,6 +786,15 @@ int zero_model_state_bytes(double psi, double nd, int32_t stage, double k, doubl
     case ZERO_STAGE_OS_G_P: *out = (params + grads + opt) / nd; break;
     default: return fail(ZERO_EINVAL, "zero_model_state_bytes: unknown stage %d", stage);
     }
+    return ZERO_OK;
+}
+
+int zero_memory_bytes(double psi, int32_t nd, int32_t stage, int32_t k, double* bytes) {
+    if (!bytes || nd < 1 || k < 0 || !(psi >= 0.0) || !is_fin(psi))
+        return fail(ZERO_EINVAL, "zero_memory_bytes: need psi >= 0 finite, nd >= 1, k >= 0 and bytes != NULL");
+    const int rc = zero_model_state_bytes(psi, (double)nd, stage, (double)k, bytes);
+    if (rc)
+        return fail(rc, "zero_memory_bytes: unknown stage %d", stage);
     return ZERO_OK;
 }
 
@@ -557,12 +827,34 @@ int zero_scaler_update(zero_scaler_t* s, int32_t skipped) {
     return ZERO_OK;
 }
 
-int zero_shard_last_stats(zero_step_stats_t* out) {
+int zero_shard_last_step_stats(zero_step_stats_t* out) {
     if (!out)
-        return fail(ZERO_EINVAL, "zero_shard_last_stats: NULL out");
+        return fail(ZERO_EINVAL, "zero_shard_last_step_stats: NULL out");
+    if (!t_have_stats)
+        return fail(ZERO_EINVAL, "zero_shard_last_step_stats: no step on this thread yet");
+    *out = t_stats;
+    return ZERO_OK;
+}
+
+int zero_shard_last_stats(double* norm, float* mult, int* overflow) {
+    if (!norm && !mult && !overflow)
+        return fail(ZERO_EINVAL, "zero_shard_last_stats: every out pointer is NULL");
     if (!t_have_stats)
         return fail(ZERO_EINVAL, "zero_shard_last_stats: no step on this thread yet");
-    *out = t_stats;
+    if (norm)
+        *norm = t_stats.norm;
+    if (mult)
+        *mult = t_stats.mult;
+    if (overflow)
+        *overflow = t_stats.overflow;
+    return ZERO_OK;
+}
+
+int zero_bias_corrections(double beta1, double beta2, int64_t step, float* bc1, float* bc2) {
+    if (!bc1 || !bc2 || step < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+        return fail(ZERO_EINVAL, "zero_bias_corrections: need beta1, beta2 in [0, 1), step >= 1, non-NULL outs");
+    *bc1 = zs::bias_correction(beta1, step);
+    *bc2 = zs::bias_correction(beta2, step);
     return ZERO_OK;
 }
 
@@ -580,46 +872,53 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
         return ZERO_OK;
     }
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     if ((rc = check_shard_ranges("zero_shard_step", grad16, master32, m32, v32, param16_out, n)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
-    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
-    const uint32_t seq = next_seq(ctx);
+    Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->info->ncu);
+    plan_small(&pl, n, ctx->info);
+    const uint32_t seq = next_seq(ctx.get());
 
     ProfRec pr{};
-    const bool prof = prof_begin(ctx, &pr);
-    if (prof && !pr.end)
-        return fail(ZERO_EHIP, "zero_shard_step: could not create a profiling event");
-    if (prof && pr.own_start)
-        HIP_TRY(hipEventRecord(pr.start, stream));
-    if ((rc = launch_stats(ctx, grad16, n, pl, loss_scale, clip, seq, stream)))
-        return rc;
+    const int prof = prof_begin(&ctx->prof_tick, &ctx->prof_epoch, &pr);
+    if (prof < 0)
+        return prof;
     if (prof)
-        HIP_TRY(hipEventRecord(pr.mid, stream));
-    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
-        return rc;
-    if (prof) {
-        HIP_TRY(hipEventRecord(pr.end, stream));
-        if ((rc = prof_end(ctx, pr)))
-            return rc;
+        prof_record(pr.start, stream, &pr);
+    if (pl.small_v) {
+        // one launch: its whole time counts as the update's
+        if (prof)
+            prof_record(pr.mid, stream, &pr);
+        rc = launch_small_into(reinterpret_cast<double*>(ctx->part), ctx->bar, &ctx->bar_count, &ctx->bar_ready,
+                               ctx->res, ctx->host_dev, grad16, master32, m32, v32, param16_out, n, pl, loss_scale,
+                               clip, seq, c, stream);
+    } else {
+        rc = launch_stats_into(ctx->info, ctx->part, ctx->res, ctx->host_dev, grad16, n, pl, loss_scale, clip, seq,
+                               stream);
+        if (!rc && prof)
+            prof_record(pr.mid, stream, &pr);
+        if (!rc)
+            rc = launch_update(ctx.get(), grad16, master32, m32, v32, param16_out, n, pl, c, stream);
     }
-    // The update kernel is already queued: wait only for the statistics and finalize kernels.
-    zs::Result r;
-    if ((rc = wait_result(ctx, seq, stream, &r)))
+    if (rc) {
+        if (prof) {
+            pr.ok = false;
+            prof_end(pr);
+        }
         return rc;
-    t_stats.sumsq = r.sumsq;
-    t_stats.norm = r.norm;
-    t_stats.coef = r.coef;
-    t_stats.mult = r.mult;
-    t_stats.overflow = r.overflow;
-    t_stats.skipped = r.skip;
-    t_stats.pad_ = 0;
-    t_stats.n = n;
-    t_have_stats = true;
+    }
+    if (prof) {
+        prof_record(pr.end, stream, &pr);
+        prof_end(pr);
+    }
+    // The update is already queued: wait only for the statistics.
+    zs::Result r;
+    if ((rc = wait_result(ctx.get(), seq, stream, &r)))
+        return rc;
+    set_stats(r, n, pl.small_v ? 1 : 0);
     return r.skip ? ZERO_SKIPPED : ZERO_OK;
 }
 
@@ -635,23 +934,21 @@ int zero_shard_stats(const uint16_t* grad16, int64_t n, double* local_sumsq, voi
         return ZERO_OK;
     }
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    int rc = get_ctx(stream, &ctx);
+    CtxLock ctx;
+    int rc = lock_ctx(stream, &ctx);
     if (rc)
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     {
         const void* ptr = grad16;
         const size_t bytes = 2 * (size_t)n;
         if ((rc = check_ranges("zero_shard_stats", &ptr, &bytes, 1)))
             return rc;
     }
-    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
-    const uint32_t seq = next_seq(ctx);
-    if ((rc = launch_stats(ctx, grad16, n, pl, 1.0, 0.0, seq, stream)))
+    const uint32_t seq = next_seq(ctx.get());
+    if ((rc = launch_stats_planned(ctx.get(), grad16, n, 1.0, 0.0, seq, stream)))
         return rc;
     zs::Result r;
-    if ((rc = wait_result(ctx, seq, stream, &r)))
+    if ((rc = wait_result(ctx.get(), seq, stream, &r)))
         return rc;
     *local_sumsq = r.sumsq;
     return ZERO_OK;
@@ -670,35 +967,36 @@ int zero_shard_apply(const uint16_t* grad16, float* master32, float* m32, float*
     if (n == 0 || overflow)
         return overflow ? ZERO_SKIPPED : ZERO_OK;
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     if ((rc = check_shard_ranges("zero_shard_apply", grad16, master32, m32, v32, param16_out, n)))
         return rc;
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
-    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
-    const uint32_t seq = next_seq(ctx);
-    // sampled timing as in zero_shard_step, unchained: the "statistics" interval
-    // here is the result-record kernel only (the statistics ran in zero_shard_stats)
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->info->ncu);
+    const uint32_t seq = next_seq(ctx.get());
+    // sampled timing as in zero_shard_step: the "statistics" interval here is the
+    // result-record kernel only (the statistics ran in zero_shard_stats)
     ProfRec pr{};
-    const bool prof = prof_begin(ctx, &pr, false);
-    if (prof && !pr.end)
-        return fail(ZERO_EHIP, "zero_shard_apply: could not create a profiling event");
-    if (prof && pr.own_start)
-        HIP_TRY(hipEventRecord(pr.start, stream));
-    zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
-    HIP_TRY(hipGetLastError());
+    const int prof = prof_begin(&ctx->prof_tick, &ctx->prof_epoch, &pr);
+    if (prof < 0)
+        return prof;
     if (prof)
-        HIP_TRY(hipEventRecord(pr.mid, stream));
-    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
-        return rc;
+        prof_record(pr.start, stream, &pr);
+    zs::k_set_result<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, seq);
+    rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "zero_shard_apply: result-record launch failed");
+    if (!rc && prof)
+        prof_record(pr.mid, stream, &pr);
+    if (!rc)
+        rc = launch_update(ctx.get(), grad16, master32, m32, v32, param16_out, n, pl, c, stream);
     if (prof) {
-        HIP_TRY(hipEventRecord(pr.end, stream));
-        if ((rc = prof_end(ctx, pr)))
-            return rc;
+        if (!rc)
+            prof_record(pr.end, stream, &pr);
+        else
+            pr.ok = false;
+        prof_end(pr);
     }
-    return ZERO_OK;
+    return rc;
 }
 
 int zero_shard_stats_async(const uint16_t* grad16, int64_t n, double* local_sumsq, void* stream_) {
@@ -713,11 +1011,10 @@ int zero_shard_stats_async(const uint16_t* grad16, int64_t n, double* local_sums
                           reinterpret_cast<uintptr_t>(local_sumsq), sizeof(double)))
         return fail(ZERO_EINVAL, "%s: local_sumsq overlaps grad16", fn);
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    int rc = get_ctx(stream, &ctx);
+    CtxLock ctx;
+    int rc = lock_ctx(stream, &ctx);
     if (rc)
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     {
         const void* ptrs[2] = {local_sumsq, grad16};
         const size_t bytes[2] = {sizeof(double), 2 * (size_t)n};
@@ -729,9 +1026,9 @@ int zero_shard_stats_async(const uint16_t* grad16, int64_t n, double* local_sums
         HIP_TRY(hipGetLastError());
         return ZERO_OK;
     }
-    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->ncu);
+    const Plan pl = plan_step(grad16, nullptr, nullptr, nullptr, nullptr, n, ctx->info->ncu);
     zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
-        <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
+        <<<pl.stats_blocks, kStatsBlock, ctx->info->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
     HIP_TRY(hipGetLastError());
     zs::k_finalize_sum<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, pl.stats_blocks, local_sumsq);
     HIP_TRY(hipGetLastError());
@@ -753,21 +1050,18 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
         return fail(ZERO_EINVAL, "%s: skipped must be 4-byte aligned", fn);
     {
         // the scalars must not alias the state the update writes
-        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
-                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
-                                reinterpret_cast<uintptr_t>(param16_out)};
-        const size_t esz[5] = {2, 4, 4, 4, 2};
+        uintptr_t a[5];
+        array_addrs(grad16, master32, m32, v32, param16_out, a);
         for (int i = 0; i < 5 && n > 0; ++i) {
-            if (overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(global_sumsq), sizeof(double)) ||
-                (skipped && overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(skipped), 4)))
+            if (overlaps(a[i], kElemSize[i] * (size_t)n, reinterpret_cast<uintptr_t>(global_sumsq), sizeof(double)) ||
+                (skipped && overlaps(a[i], kElemSize[i] * (size_t)n, reinterpret_cast<uintptr_t>(skipped), 4)))
                 return fail(ZERO_EINVAL, "%s: global_sumsq or skipped overlaps array %d", fn, i);
         }
     }
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
+    CtxLock ctx;
+    if ((rc = lock_ctx(stream, &ctx)))
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     {
         const void* ptrs[2] = {global_sumsq, skipped};
         const size_t bytes[2] = {sizeof(double), sizeof(int32_t)};
@@ -776,31 +1070,60 @@ int zero_shard_apply_async(const uint16_t* grad16, float* master32, float* m32, 
     }
     if (n > 0 && (rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
         return rc;
-    const uint32_t seq = next_seq(ctx);
+    const uint32_t seq = next_seq(ctx.get());
     if (n == 0) {
         zs::k_set_result_dev<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, skipped, seq);
         HIP_TRY(hipGetLastError());
         return ZERO_OK;
     }
     const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
-    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->info->ncu);
     ProfRec pr{};
-    const bool prof = prof_begin(ctx, &pr, false);  // unchained, as zero_shard_apply
-    if (prof && !pr.end)
-        return fail(ZERO_EHIP, "%s: could not create a profiling event", fn);
+    const int prof = prof_begin(&ctx->prof_tick, &ctx->prof_epoch, &pr);  // timed as zero_shard_apply
+    if (prof < 0)
+        return prof;
     if (prof)
-        HIP_TRY(hipEventRecord(pr.start, stream));
+        prof_record(pr.start, stream, &pr);
     zs::k_set_result_dev<<<1, 64, 0, stream>>>(ctx->res, global_sumsq, loss_scale, clip, skipped, seq);
-    HIP_TRY(hipGetLastError());
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.mid, stream));
-    if ((rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, c, stream)))
-        return rc;
+    rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "%s: result-record launch failed", fn);
+    if (!rc && prof)
+        prof_record(pr.mid, stream, &pr);
+    if (!rc)
+        rc = launch_update(ctx.get(), grad16, master32, m32, v32, param16_out, n, pl, c, stream);
     if (prof) {
-        HIP_TRY(hipEventRecord(pr.end, stream));
-        if ((rc = prof_end(ctx, pr)))
-            return rc;
+        if (!rc)
+            prof_record(pr.end, stream, &pr);
+        else
+            pr.ok = false;
+        prof_end(pr);
     }
+    return rc;
+}
+
+int zero_resident_state_init(zero_resident_state_t* out, double lr, double beta1, double beta2, double eps,
+                             double weight_decay, double clip, double loss_scale, double min_scale, int64_t window,
+                             int64_t t) {
+    const char* fn = "zero_resident_state_init";
+    if (!out)
+        return fail(ZERO_EINVAL, "%s: NULL out", fn);
+    int rc = check_hyper(fn, lr, beta1, beta2, eps, weight_decay, t, loss_scale, clip);
+    if (rc)
+        return rc;
+    if (!is_fin(min_scale) || !(min_scale > 0.0))
+        return fail(ZERO_EINVAL, "%s: min_scale must be finite and > 0", fn);
+    zero_resident_state_t s;
+    std::memset(&s, 0, sizeof s);
+    s.lr = lr;
+    s.beta1 = beta1;
+    s.beta2 = beta2;
+    s.eps = eps;
+    s.weight_decay = weight_decay;
+    s.clip = clip;
+    s.loss_scale = loss_scale;
+    s.min_scale = min_scale;
+    s.window = window;
+    s.t = t;
+    *out = s;
     return ZERO_OK;
 }
 
@@ -813,19 +1136,17 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
     if (!state || reinterpret_cast<uintptr_t>(state) % 8)
         return fail(ZERO_EINVAL, "%s: state must be an 8-byte aligned device pointer", fn);
     {
-        const uintptr_t a[5] = {reinterpret_cast<uintptr_t>(grad16), reinterpret_cast<uintptr_t>(master32),
-                                reinterpret_cast<uintptr_t>(m32), reinterpret_cast<uintptr_t>(v32),
-                                reinterpret_cast<uintptr_t>(param16_out)};
-        const size_t esz[5] = {2, 4, 4, 4, 2};
+        uintptr_t a[5];
+        array_addrs(grad16, master32, m32, v32, param16_out, a);
         for (int i = 0; i < 5 && n > 0; ++i)
-            if (overlaps(a[i], esz[i] * (size_t)n, reinterpret_cast<uintptr_t>(state), sizeof *state))
+            if (overlaps(a[i], kElemSize[i] * (size_t)n, reinterpret_cast<uintptr_t>(state), sizeof *state))
                 return fail(ZERO_EINVAL, "%s: state overlaps array %d", fn, i);
     }
     hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-    Ctx* ctx = nullptr;
-    if ((rc = get_ctx(stream, &ctx)))
+    int dev = 0;
+    const DevInfo* info = nullptr;
+    if ((rc = current_device(stream, &dev)) || (rc = dev_info(dev, &info)))
         return rc;
-    std::lock_guard<std::mutex> lk(ctx->mu);
     // While the stream is being captured into a graph only kernel launches are
     // recorded: the allocation lookups and the sampled timing run on eager calls.
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -839,34 +1160,102 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
         if (n > 0 && (rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
             return rc;
     }
-    const uint32_t seq = next_seq(ctx);
-    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, ctx->ncu);
+    ResWs* ws = nullptr;
+    if ((rc = resident_ws(dev, state, stream, &ws)))
+        return rc;
+    if (++ws->seq == 0)
+        ++ws->seq;
+    const uint32_t seq = ws->seq;
+    const Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, info->ncu);
     ProfRec pr{};
-    const bool prof = !capturing && n > 0 && prof_begin(ctx, &pr, false);
-    if (prof && !pr.end)
-        return fail(ZERO_EHIP, "%s: could not create a profiling event", fn);
+    const int prof = !capturing && n > 0 ? prof_begin(&ws->prof_tick, &ws->prof_epoch, &pr) : 0;
+    if (prof < 0)
+        return prof;
     if (prof)
-        HIP_TRY(hipEventRecord(pr.start, stream));
+        prof_record(pr.start, stream, &pr);
     // statistics, then one workgroup that totals them, fills the result record and the
     // constants and advances the state record's loss-scale schedule (an empty shard has no
     // partials: its total is 0), then the update
     if (n > 0) {
         zs::k_stats<kStatsBlock, kStatsUnroll, kStatsNTL, kStatsXCD>
-            <<<pl.stats_blocks, kStatsBlock, ctx->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ctx->part);
-        HIP_TRY(hipGetLastError());
+            <<<pl.stats_blocks, kStatsBlock, info->stats_lds, stream>>>(grad16, n, pl.ghead, pl.gvec, ws->part);
+        rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "%s: statistics launch failed", fn);
     }
-    zs::k_resident_begin<<<1, zs::kFinalBlock, 0, stream>>>(ctx->part, n > 0 ? pl.stats_blocks : 0, state, ctx->res,
-                                                            ctx->dconst, seq);
-    HIP_TRY(hipGetLastError());
-    if (prof)
-        HIP_TRY(hipEventRecord(pr.mid, stream));
-    if (n > 0 && (rc = launch_update(ctx, grad16, master32, m32, v32, param16_out, n, pl, zs::AdamConst{}, stream,
-                                     ctx->dconst)))
-        return rc;
+    if (!rc) {
+        zs::k_resident_begin<<<1, zs::kFinalBlock, 0, stream>>>(ws->part, n > 0 ? pl.stats_blocks : 0, state,
+                                                                ws->res, ws->dconst, seq);
+        rc = hipGetLastError() == hipSuccess ? ZERO_OK : fail(ZERO_EHIP, "%s: record kernel launch failed", fn);
+    }
+    if (!rc && prof)
+        prof_record(pr.mid, stream, &pr);
+    if (!rc && n > 0)
+        rc = launch_update_from(info, ws->res, grad16, master32, m32, v32, param16_out, n, pl, zs::AdamConst{},
+                                stream, ws->dconst);
     if (prof) {
-        HIP_TRY(hipEventRecord(pr.end, stream));
-        if ((rc = prof_end(ctx, pr)))
-            return rc;
+        if (!rc)
+            prof_record(pr.end, stream, &pr);
+        else
+            pr.ok = false;
+        prof_end(pr);
+    }
+    return rc;
+}
+
+int zero_resident_release(const zero_resident_state_t* state) {
+    if (!state)
+        return fail(ZERO_EINVAL, "zero_resident_release: NULL state");
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    std::lock_guard<std::mutex> lk(g_res_mu);
+    auto it = g_res.find(std::make_pair(dev, static_cast<const void*>(state)));
+    if (it == g_res.end())
+        return ZERO_OK;
+    // replays of captured graphs may use the workspace on any stream of the device
+    HIP_TRY(hipDeviceSynchronize());
+    free_res_ws(&it->second);
+    g_res.erase(it);
+    return ZERO_OK;
+}
+
+int zero_stream_release(void* stream_) {
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    int dev = 0;
+    int rc = current_device(stream, &dev);
+    if (rc)
+        return rc;
+    std::shared_ptr<Ctx> c;
+    {
+        std::lock_guard<std::mutex> lk(g_ctx_mu);
+        auto it = g_ctx.find(std::make_pair(dev, stream));
+        if (it == g_ctx.end())
+            return ZERO_OK;
+        c = it->second;
+    }
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (c->released)
+        return ZERO_OK;
+    HIP_TRY(hipStreamSynchronize(stream));
+    {
+        std::lock_guard<std::mutex> glk(g_ctx_mu);
+        auto it = g_ctx.find(std::make_pair(dev, stream));
+        if (it != g_ctx.end() && it->second == c)
+            g_ctx.erase(it);
+    }
+    c->released = true;
+    free_ctx_buffers(c.get());
+    return ZERO_OK;
+}
+
+int zero_workspace_count(int64_t* streams, int64_t* records) {
+    if (!streams && !records)
+        return fail(ZERO_EINVAL, "zero_workspace_count: every out pointer is NULL");
+    if (streams) {
+        std::lock_guard<std::mutex> lk(g_ctx_mu);
+        *streams = (int64_t)g_ctx.size();
+    }
+    if (records) {
+        std::lock_guard<std::mutex> lk(g_res_mu);
+        *records = (int64_t)g_res.size();
     }
     return ZERO_OK;
 }
@@ -890,10 +1279,7 @@ int zero_profile_enable(int32_t every) {
         return fail(ZERO_EINVAL, "zero_profile_enable: every must be >= 0");
     std::lock_guard<std::mutex> lk(g_prof_mu);
     g_prof_every = every;
-    prof_forget_ends();
-    std::lock_guard<std::mutex> lk2(g_ctx_mu);
-    for (auto& kv : g_ctx)
-        kv.second->prof_tick = 0;
+    g_prof_epoch += 1;  // every stream restarts its sampling count
     return ZERO_OK;
 }
 
@@ -901,12 +1287,11 @@ int zero_profile_read(zero_profile_t* out) {
     if (!out)
         return fail(ZERO_EINVAL, "zero_profile_read: NULL out");
     std::lock_guard<std::mutex> lk(g_prof_mu);
-    int rc = prof_drain_locked();
-    if (rc)
-        return rc;
+    prof_drain_locked();
+    const int rc = prof_take_error(0);
     *out = g_prof_acc;
     g_prof_acc = zero_profile_t{0, 0.0, 0.0};
-    return ZERO_OK;
+    return rc;
 }
 
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {

@@ -34,6 +34,12 @@ int zo_lamb_step(const uint16_t* g16, float* theta, float* m, float* v, uint16_t
                  const int64_t* seg_off, int32_t n_seg, double lr, double beta1, double beta2, double eps,
                  double wd, int64_t t, double loss_scale, double clip, double phi_lo, double phi_hi,
                  void* scalars_out, double* seg_out);
+/* The oracle's model-state accounting and fp32 update constants. */
+double zo_model_state_bytes(double psi, double nd, int32_t stage, double k);
+typedef struct {
+    float lr, b1, omb1, b2, omb2, bc1, bc2, eps, wd;
+} zo_hyper_t;
+void zo_hyper(double lr, double beta1, double beta2, double eps, double wd, int64_t t, zo_hyper_t* h);
 
 #define LR 1e-4
 #define B1 0.9
@@ -156,8 +162,17 @@ static int run_case(int64_t n, const int shift[5], hipStream_t stream) {
             break;
         }
         zero_step_stats_t st;
-        if (n > 0 && (zero_shard_last_stats(&st) != ZERO_OK || st.skipped != want || st.n != n)) {
+        if (n > 0 && (zero_shard_last_step_stats(&st) != ZERO_OK || st.skipped != want || st.n != n)) {
             printf("FAIL: %s: last stats disagree (skipped %d, n %lld)\n", what, st.skipped, (long long)st.n);
+            ok = 0;
+            break;
+        }
+        double norm = -1.0;
+        float mult = -1.0f;
+        int ovf = -1;
+        if (n > 0 && (zero_shard_last_stats(&norm, &mult, &ovf) != ZERO_OK || ovf != want ||
+                      memcmp(&norm, &st.norm, sizeof norm) != 0 || memcmp(&mult, &st.mult, sizeof mult) != 0)) {
+            printf("FAIL: %s: three-pointer last stats disagree with the record\n", what);
             ok = 0;
             break;
         }
@@ -271,7 +286,47 @@ static int run_lamb_case(int64_t n, const int shift[5], hipStream_t stream) {
     return ok;
 }
 
+/* Host-only entry points against the oracle (no GPU needed): the accounting of
+ * every Table 1 cell's parameters and the bias corrections of the first 2000
+ * steps of two Adam settings. */
+static int host_checks(void) {
+    const double psis[3] = {7.5e9, 128e9, 1e12};
+    const int32_t nds[6] = {1, 4, 16, 64, 256, 1024};
+    for (int a = 0; a < 3; ++a)
+        for (int b = 0; b < 6; ++b)
+            for (int32_t st = ZERO_STAGE_DP; st <= ZERO_STAGE_OS_G_P; ++st) {
+                double got = -1.0;
+                const double want = zo_model_state_bytes(psis[a], (double)nds[b], st, 12.0);
+                if (zero_memory_bytes(psis[a], nds[b], st, 12, &got) != ZERO_OK || got != want) {
+                    printf("FAIL: zero_memory_bytes(%g, %d, %d, 12) = %.17g, oracle %.17g\n", psis[a], nds[b], st,
+                           got, want);
+                    return 0;
+                }
+            }
+    if (zero_memory_bytes(1e9, 0, ZERO_STAGE_OS, 12, NULL) != ZERO_EINVAL) {
+        printf("FAIL: zero_memory_bytes accepted nd = 0 and a NULL out\n");
+        return 0;
+    }
+    const double betas[2][2] = {{0.9, 0.999}, {0.95, 0.98}};
+    for (int k = 0; k < 2; ++k)
+        for (int64_t t = 1; t <= 2000; ++t) {
+            float bc1 = 0.f, bc2 = 0.f;
+            zo_hyper_t h;
+            zo_hyper(LR, betas[k][0], betas[k][1], 1e-8, 0.0, t, &h);
+            if (zero_bias_corrections(betas[k][0], betas[k][1], t, &bc1, &bc2) != ZERO_OK ||
+                memcmp(&bc1, &h.bc1, sizeof bc1) != 0 || memcmp(&bc2, &h.bc2, sizeof bc2) != 0) {
+                printf("FAIL: bias corrections at betas (%g, %g), t = %lld differ from the oracle\n", betas[k][0],
+                       betas[k][1], (long long)t);
+                return 0;
+            }
+        }
+    printf("host checks ok\n");
+    return 1;
+}
+
 int main(void) {
+    if (!host_checks())
+        return 1;
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || ndev < 1) {
         printf("no GPU\n");
@@ -297,6 +352,10 @@ int main(void) {
     for (size_t k = 0; k < sizeof lamb_sizes / sizeof lamb_sizes[0] && ok; ++k)
         ok = run_lamb_case(lamb_sizes[k], aligned, stream) && run_lamb_case(lamb_sizes[k], equal, stream) &&
              run_lamb_case(lamb_sizes[k], mixed, stream);
+    if (zero_stream_release(stream) != ZERO_OK) {
+        printf("FAIL: zero_stream_release: %s\n", zero_last_error());
+        ok = 0;
+    }
     HIPCHECK(hipStreamDestroy(stream));
     printf(ok ? "c-abi driver: all cases match the oracle\n" : "c-abi driver: FAILED\n");
     return ok ? 0 : 1;

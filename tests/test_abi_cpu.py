@@ -127,7 +127,7 @@ def test_step_rejects_invalid_arguments(zb, kw, ptrs, n):
 
 def test_step_with_zero_elements_is_a_noop(zb):
     assert _step_raw(zb, [0, 0, 0, 0, 0], 0) == zb.ZERO_OK
-    st = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
     assert st.n == 0 and st.skipped == 0
 
 
@@ -324,3 +324,132 @@ def test_resident_step_rejects_without_a_gpu(zb):
     assert lib.zero_shard_step_resident(G[0] + 1, *G[1:], 10, 0x60000000, None) == zb.ZERO_EINVAL
     assert lib.zero_shard_step_resident(*G, -1, 0x60000000, None) == zb.ZERO_EINVAL
     assert "state" in zb.zero_last_error() or "n=" in zb.zero_last_error()
+
+
+# ---------------------------------------------------------------------------
+# The boundary's helper calls as the scope table declares them
+# ---------------------------------------------------------------------------
+
+def _table1_cells():
+    gold = os.path.join(ROOT, "tests", "golden", "table1_memory.txt")
+    models = [7.5e9, 128e9, 1e12]
+    stages = [zb_stage for zb_stage in (1, 2, 3)]
+    with open(gold) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                row = line.split()
+                for j, printed in enumerate(row[1:]):
+                    yield int(row[0]), models[j // 3], stages[j % 3], printed
+
+
+def test_memory_bytes_on_every_table1_cell(zb):
+    # Sec. 5.2, Table 1 (K = 12): each printed cell within one unit of its last digit, and
+    # the value equal to the oracle's accounting
+    cells = list(_table1_cells())
+    assert len(cells) == 54
+    for nd, psi, stage, printed in cells:
+        got = zb.zero_memory_bytes(psi, nd, stage, 12)
+        unit = 10.0 ** -len(printed.split(".")[1]) if "." in printed else 1.0
+        assert abs(got / 1e9 - float(printed)) < unit, (nd, psi, stage, got, printed)
+        assert got == oracle.model_state_bytes(psi, nd, stage)
+    assert zb.zero_memory_bytes(7.5e9, 64, zb.ZERO_STAGE_DP, 12) == oracle.model_state_bytes(7.5e9, 64, 0)
+
+
+def test_memory_bytes_rejects(zb):
+    lib = zb.raw_library()
+    out = ctypes.c_double()
+    assert lib.zero_memory_bytes(1e9, 0, 1, 12, ctypes.byref(out)) == zb.ZERO_EINVAL
+    assert lib.zero_memory_bytes(1e9, 4, 1, -1, ctypes.byref(out)) == zb.ZERO_EINVAL
+    assert lib.zero_memory_bytes(-1.0, 4, 1, 12, ctypes.byref(out)) == zb.ZERO_EINVAL
+    assert lib.zero_memory_bytes(float("nan"), 4, 1, 12, ctypes.byref(out)) == zb.ZERO_EINVAL
+    assert lib.zero_memory_bytes(1e9, 4, 7, 12, ctypes.byref(out)) == zb.ZERO_EINVAL
+    assert lib.zero_memory_bytes(1e9, 4, 1, 12, None) == zb.ZERO_EINVAL
+
+
+def test_last_stats_three_pointer_form(zb):
+    lib = zb.raw_library()
+    # an empty step (no GPU work) sets the thread's statistics: norm 0, mult 1/scale, no overflow
+    assert _step_raw(zb, [0, 0, 0, 0, 0], 0, scale=1024.0) == zb.ZERO_OK
+    norm, mult, ovf = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
+    assert (norm, mult, ovf) == (0.0, np.float32(1.0 / 1024.0), 0)
+    assert (norm, mult, ovf) == (st.norm, st.mult, st.overflow)
+    only = ctypes.c_int(-1)
+    assert lib.zero_shard_last_stats(None, None, ctypes.byref(only)) == zb.ZERO_OK and only.value == 0
+    assert lib.zero_shard_last_stats(None, None, None) == zb.ZERO_EINVAL
+
+
+def _exact_bias_correction_f32(beta, tmax):
+    """fp32(1 - RN64(beta^t)) for t = 1..tmax from the exact power: beta is a dyadic
+    rational, so beta^t is carried in 400-bit fixed point (truncation error below
+    t * 2^-400) and rounded to the nearest double with the remainder as sticky bits
+    (below 2^-60 the difference 1 - beta^t rounds to 1 whatever the power's bits)."""
+    from fractions import Fraction
+    prec = 400
+    b = Fraction(beta)
+    B = (b.numerator << prec) // b.denominator
+    assert Fraction(B, 1 << prec) == b
+    P = 1 << prec
+    out = np.empty(tmax, np.float32)
+    for t in range(1, tmax + 1):
+        P = (P * B) >> prec
+        if P.bit_length() <= prec - 60:   # beta^t < 2^-60: 1 - beta^t rounds to 1 in double
+            out[t - 1] = np.float32(1.0)
+            continue
+        drop = P.bit_length() - 53
+        mant, rem = P >> drop, P & ((1 << drop) - 1)
+        half = 1 << (drop - 1)
+        if rem > half or (rem == half and (mant & 1)):
+            mant += 1
+        out[t - 1] = np.float32(1.0 - float(np.ldexp(float(mant), drop - prec)))
+    return out
+
+
+@pytest.mark.parametrize("beta1,beta2", [(0.9, 0.98), (0.9, 0.999), (0.9, 0.9999), (0.95, 0.98), (0.95, 0.999),
+                                         (0.95, 0.9999)])
+def test_bias_corrections_match_the_exact_power_and_the_oracle(zb, beta1, beta2):
+    # Adam's bias corrections 1 - beta^t (Kingma & Ba, cited in Sec. 3.1): the library's one
+    # definition (the host calls and the resident kernel share it) against the exact power,
+    # and against the oracle's C-library pow, for t = 1..20000
+    tmax = 20000
+    ex1, ex2 = _exact_bias_correction_f32(beta1, tmax), _exact_bias_correction_f32(beta2, tmax)
+    lib = zb.raw_library()
+    a, b = ctypes.c_float(), ctypes.c_float()
+    for t in range(1, tmax + 1):
+        assert lib.zero_bias_corrections(beta1, beta2, t, ctypes.byref(a), ctypes.byref(b)) == zb.ZERO_OK
+        h = oracle.hyper(1e-4, beta1, beta2, 1e-8, 0.0, t)
+        assert np.float32(a.value) == ex1[t - 1] == np.float32(h.bc1), (t, a.value, ex1[t - 1], h.bc1)
+        assert np.float32(b.value) == ex2[t - 1] == np.float32(h.bc2), (t, b.value, ex2[t - 1], h.bc2)
+
+
+def test_bias_corrections_rejects(zb):
+    lib = zb.raw_library()
+    a, b = ctypes.c_float(), ctypes.c_float()
+    assert lib.zero_bias_corrections(1.0, 0.9, 1, ctypes.byref(a), ctypes.byref(b)) == zb.ZERO_EINVAL
+    assert lib.zero_bias_corrections(0.9, -0.1, 1, ctypes.byref(a), ctypes.byref(b)) == zb.ZERO_EINVAL
+    assert lib.zero_bias_corrections(0.9, 0.99, 0, ctypes.byref(a), ctypes.byref(b)) == zb.ZERO_EINVAL
+    assert lib.zero_bias_corrections(0.9, 0.99, 1, None, ctypes.byref(b)) == zb.ZERO_EINVAL
+    # beta = 0: 1 - 0^t = 1 at every t
+    assert zb.zero_bias_corrections(0.0, 0.0, 7) == (1.0, 1.0)
+
+
+def test_resident_state_init_checks_the_record(zb):
+    ok = dict(lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, clip=1.0, loss_scale=65536.0,
+              min_scale=1.0, window=1000, t=1)
+    st = zb.resident_state_record(**ok)
+    assert (st.t, st.good, st.steps, st.skipped, st.loss_scale, st.window) == (1, 0, 0, 0, 65536.0, 1000)
+    for bad in (dict(t=0), dict(beta1=1.0), dict(beta2=-0.5), dict(loss_scale=0.0), dict(loss_scale=float("inf")),
+                dict(min_scale=0.0), dict(min_scale=float("nan")), dict(lr=-1.0), dict(eps=float("nan")),
+                dict(clip=float("nan")), dict(weight_decay=float("inf"))):
+        with pytest.raises(zb.ZeroError) as e:
+            zb.resident_state_record(**dict(ok, **bad))
+        assert e.value.code == zb.ZERO_EINVAL, bad
+    assert zb.raw_library().zero_resident_state_init(None, 1e-4, 0.9, 0.999, 1e-8, 0.0, 1.0, 65536.0, 1.0, 1000,
+                                                     1) == zb.ZERO_EINVAL
+
+
+def test_workspace_count_without_a_gpu(zb):
+    assert zb.zero_workspace_count() == (0, 0)
+    assert zb.raw_library().zero_workspace_count(None, None) == zb.ZERO_EINVAL
+    assert zb.raw_library().zero_resident_release(None) == zb.ZERO_EINVAL

@@ -3,7 +3,9 @@ runtime API for memory and streams, libzeroshard for the shard step, the C
 oracle for the expected bytes -- no Python or PyTorch in the process.
 
 CPU: the program compiles warning-free against include/zero_shard.h, links the
-library and the oracle, and reports that no GPU is present.  GPU: every case
+library and the oracle, checks the host-only entry points against the oracle
+(the accounting of every Table 1 cell's parameters, the bias corrections of
+2000 steps) and reports that no GPU is present.  GPU: every case
 (several shard lengths, aligned / equally shifted / unequally shifted arrays,
 a skipped step, the split phase, a created stream and the null stream)
 matches the oracle byte for byte."""
@@ -42,7 +44,8 @@ def test_c_driver_builds_and_needs_a_gpu(tmp_path):
     if torch.cuda.is_available():
         pytest.skip("a GPU is present: the GPU test runs the driver")
     r = subprocess.run([exe], stdout=subprocess.PIPE, stderr=subprocess.STDOUT, timeout=60)
-    assert r.returncode == 77, r.stdout.decode(errors="replace")
+    out = r.stdout.decode(errors="replace")
+    assert r.returncode == 77 and "host checks ok" in out, out
 
 
 @pytest.mark.gpu

@@ -47,7 +47,7 @@ def _check_step(env, plan, bufs, ref, g16, seg, hp, t, scale, clip, phi=(0.0, fl
     bufs[0].upload(g16)
     flag = zb.zero_lamb_step(plan, *(b.view for b in bufs), hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
                              hp["wd"], t, scale, clip, phi[0], phi[1])
-    st = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
     torch.cuda.synchronize()
     skip, sc, _ = H.oracle_lamb_step(g16, *ref, seg, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t,
                                      scale, clip, phi[0], phi[1])

@@ -65,7 +65,7 @@ def test_lamb_shard_beyond_int32_range():
     with zb.LambPlan(seg) as plan:
         flag = zb.zero_lamb_step(plan, *d, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], HP["wd"], 1,
                                  w.loss_scale, w.clip)
-        st = zb.zero_shard_last_stats()
+        st = zb.zero_shard_last_step_stats()
         torch.cuda.synchronize()
     assert flag == 0 and abs(st.norm / sc.norm - 1) <= 1e-9
     hp = oracle.hyper(HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], HP["wd"], 1)

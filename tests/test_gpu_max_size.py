@@ -50,7 +50,7 @@ def test_shard_beyond_int32_range():
     d.append(torch.full((N,), workloads.P16_SENTINEL, dtype=torch.int16, device=dev).view(torch.float16))
     say("step")
     flag = zb.zero_shard_step(*d, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay, 1, w.loss_scale, w.clip)
-    st = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
     torch.cuda.synchronize()
     assert flag == 0 and abs(st.norm / sc.norm - 1) <= 1e-9
     ti = torch.from_numpy(idx).to(dev)

@@ -58,7 +58,7 @@ def _run_case(env, g16_steps, theta, m, v, hp, scales=None, shifts=(0, 0, 0, 0, 
         say(label, "step", k + 1, "n", n, "shifts", shifts)
         flag = zb.zero_shard_step(bufs[0].view, bufs[1].view, bufs[2].view, bufs[3].view, bufs[4].view,
                                   hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t, scale, clip)
-        st = zb.zero_shard_last_stats()
+        st = zb.zero_shard_last_step_stats()
         torch.cuda.synchronize()
         skip, sc = H.oracle_step(g16, *ref, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t, scale, clip)
         assert flag == skip and st.skipped == skip and st.overflow == skip
@@ -104,7 +104,7 @@ def _run_workload(env, key, steps=None, rank=None):
         say(key, "step", step, "t", t, "scale", scale)
         flag = zb.zero_shard_step(bufs[0].view, bufs[1].view, bufs[2].view, bufs[3].view, bufs[4].view,
                                   hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t, scale, w.clip)
-        st = zb.zero_shard_last_stats()
+        st = zb.zero_shard_last_step_stats()
         torch.cuda.synchronize()
         skip, sc = H.oracle_step(g16, *ref, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["wd"], t, scale, w.clip)
         assert flag == skip, (step, flag, skip)
@@ -207,7 +207,7 @@ def test_overflow_skips_and_touches_nothing(env, where, pattern):
                               1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 2.0 ** 16, 1.0)
     torch.cuda.synchronize()
     assert flag == 1
-    st = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
     assert st.overflow == 1 and st.skipped == 1
     for b, a in zip(bufs[1:], (theta, m, v, workloads.p16_sentinel(n))):
         got = b.download()
@@ -227,7 +227,7 @@ def test_deterministic_run_to_run(env):
         say("determinism rep", rep)
         zb.zero_shard_step(bufs[0].view, bufs[1].view, bufs[2].view, bufs[3].view, bufs[4].view,
                            1e-4, 0.9, 0.999, 1e-8, 0.0, 1, 2.0 ** 16, 1.0)
-        st = zb.zero_shard_last_stats()
+        st = zb.zero_shard_last_step_stats()
         torch.cuda.synchronize()
         outs.append(([b.download().copy() for b in bufs[1:]], st.sumsq, st.mult))
     for a, b in zip(outs[0][0], outs[1][0]):

@@ -64,7 +64,7 @@ def test_split_equals_fused_step(env):
     say("fused step vs stats+apply, n", n)
     f1 = zb.zero_shard_step(*(x.view for x in a), HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], HP["weight_decay"],
                             1, 2.0 ** 16, 1.0)
-    st = zb.zero_shard_last_stats()
+    st = zb.zero_shard_last_step_stats()
     local = zb.zero_shard_stats(b[0].view)
     f2 = zb.zero_shard_apply(*(x.view for x in b), local, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
                              HP["weight_decay"], 1, 2.0 ** 16, 1.0)
