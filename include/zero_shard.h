@@ -109,11 +109,15 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
  * the vectorised path runs after a few scalar head elements).  Placement
  * affects speed, not results: separate allocations, or arrays packed into one
  * buffer each on its own 2 MiB boundary, run fastest; arrays offset from one
- * another by a few hundred bytes run about 5 % slower.  Shards of up to 2^22
- * elements whose arrays share one misalignment take a single cooperative
- * launch (statistics, a grid barrier and the update in one kernel, the
- * gradient read once); larger ones take the statistics kernels and the update
- * kernel.  The call
+ * another by a few hundred bytes run about 5 % slower.  Shards small enough
+ * for one resident grid (a quarter of the device's co-resident capacity for
+ * the kernel: about 1.5 million elements on MI355X) whose arrays share one
+ * misalignment take a single launch (statistics, a grid barrier and the
+ * update in one kernel, the gradient read once); larger ones take the
+ * statistics kernels and the update kernel.  The barrier relies on the whole
+ * grid being resident at once; its wait is bounded, and should the device
+ * not run the grid together within seconds, the step writes nothing and
+ * returns ZERO_EHIP.  The call
  * blocks until the skip decision is known (the statistics kernels publish it
  * in host-mapped memory, which the calling thread polls); the update kernel
  * may still be running on `stream` when it returns.  Returns 0 applied,

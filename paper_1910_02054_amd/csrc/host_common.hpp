@@ -41,8 +41,7 @@ struct DevInfo {
     int ncu = 0;
     size_t stats_lds = 0, adam_lds = 0;
     int stats_resident = 0, adam_resident = 0;
-    int64_t small_cap[4] = {0, 0, 0, 0};  // co-resident workgroups of k_small_step<1, 2, 4, 8>
-                                          // (0: no cooperative launch on this device)
+    int64_t small_cap[4] = {};  // co-resident workgroups of k_small_step<1, 2, 4, 8>
 };
 
 // The facts of device `dev` (0 <= dev < kMaxDevices), filled on first use.
@@ -64,9 +63,8 @@ struct Ctx {
     zs::Result* res = nullptr;      // result record (device), read by the update kernel
     zs::Result* host = nullptr;     // host-mapped, GPU-uncached copy of the result record
     zs::Result* host_dev = nullptr; // its device-side address
-    uint64_t* bar = nullptr;        // grid-barrier counter of the small-shard step (device)
-    uint64_t bar_count = 0;         // arrivals the counter has received so far
-    bool bar_ready = false;         // the counter has been zeroed on the stream
+    uint64_t* sync = nullptr;       // grid-barrier words of the small-shard step (device)
+    bool sync_ready = false;        // the words have been zeroed on the stream
     uint64_t prof_tick = 0;         // steps seen while profiling (for sampling)
     uint64_t prof_epoch = 0;        // profiling period the tick belongs to
     uint32_t seq = 0;               // call counter echoed in the result record

@@ -18,11 +18,10 @@
 //               device memory and to a host-mapped record.
 //   k_adam_*    the fused update: unscale+clip, Adam with bias correction, fp16
 //               cast; 14 bytes read and 14 bytes written per element.
-// Small shards take one cooperative launch instead (k_small_step): every
-// thread keeps its elements in registers, the workgroups meet at a grid
-// barrier after the statistics, each totals the partials in the same fixed
-// order, and the update follows from the registers (28 bytes per element, one
-// launch).
+// Small shards take one launch instead (k_small_step): every thread keeps
+// its elements in registers, the workgroups meet at a grid barrier after the
+// statistics, each totals the partials in the same fixed order, and the update
+// follows from the registers (28 bytes per element, one launch).
 // The other ways of running the same step swap only the one-thread kernels
 // around these: the split phase takes the global sum from the host
 // (k_set_result) or from device memory (k_finalize_sum writes a rank's local
@@ -341,10 +340,10 @@ __device__ __forceinline__ double partials_total(const Partial* __restrict__ par
         *out = value;
 }
 
-// One 64-bit word into device memory (a counter cleared in stream order).
-[[maybe_unused]] static __global__ __launch_bounds__(64) void k_set_u64(uint64_t* __restrict__ out, uint64_t value) {
-    if (threadIdx.x == 0)
-        *out = value;
+// Zeroes n 64-bit words (counters cleared in stream order).
+[[maybe_unused]] static __global__ __launch_bounds__(256) void k_zero_words(uint64_t* __restrict__ out, int64_t n) {
+    for (int64_t i = threadIdx.x; i < n; i += 256)
+        out[i] = 0;
 }
 
 // Statistics total into caller device memory (the asynchronous split phase:
@@ -385,37 +384,44 @@ __device__ __forceinline__ double partials_total(const Partial* __restrict__ par
 // result record and the constants, so the schedule need not wait for it.  A
 // record outside the accepted ranges (resident_record_ok) is left unchanged
 // except for skipped = -1, and the step writes nothing.
+// The resident step's decision from the statistics total and the record `s`
+// read before the step: the result record, and the record's new scaler fields
+// written to *st (skipped = -1 and nothing else for a record out of range).
+__device__ __forceinline__ Result resident_advance(zero_resident_state_t* __restrict__ st,
+                                                   const zero_resident_state_t& s, double tot, uint32_t seq) {
+    if (!resident_record_ok(s)) {
+        Result r = make_result(0.0, 1.0, 0.0, seq);
+        r.skip = 1;
+        st->skipped = -1;
+        return r;
+    }
+    const Result r = make_result(tot, s.loss_scale, s.clip, seq);
+    st->steps = s.steps + 1;
+    st->skipped = r.skip;
+    if (r.skip) {
+        const double h = s.loss_scale * 0.5;
+        st->loss_scale = h > s.min_scale ? h : s.min_scale;
+        st->good = 0;
+    } else {
+        st->t = s.t + 1;
+        int64_t good = s.good + 1;
+        if (s.window > 0 && good >= s.window) {
+            st->loss_scale = s.loss_scale * 2.0;
+            good = 0;
+        }
+        st->good = good;
+    }
+    return r;
+}
+
 [[maybe_unused]] static __global__ __launch_bounds__(kFinalBlock) void k_resident_begin(
     const Partial* __restrict__ part, int nparts, zero_resident_state_t* __restrict__ st, Result* __restrict__ res,
     AdamConst* __restrict__ cout, uint32_t seq) {
     const double tot = partials_total(part, nparts);
     if (threadIdx.x == 0) {
         const zero_resident_state_t s = *st;
-        if (!resident_record_ok(s)) {
-            Result r = make_result(0.0, 1.0, 0.0, seq);
-            r.skip = 1;
-            *res = r;
-            st->skipped = -1;
-            return;
-        }
-        const Result r = make_result(tot, s.loss_scale, s.clip, seq);
-        *res = r;
         *cout = make_adam_const(s.lr, s.beta1, s.beta2, s.eps, s.weight_decay, s.t);
-        st->steps = s.steps + 1;
-        st->skipped = r.skip;
-        if (r.skip) {
-            const double h = s.loss_scale * 0.5;
-            st->loss_scale = h > s.min_scale ? h : s.min_scale;
-            st->good = 0;
-        } else {
-            st->t = s.t + 1;
-            int64_t good = s.good + 1;
-            if (s.window > 0 && good >= s.window) {
-                st->loss_scale = s.loss_scale * 2.0;
-                good = 0;
-            }
-            st->good = good;
-        }
+        *res = resident_advance(st, s, tot, seq);
     }
 }
 
@@ -550,43 +556,122 @@ __global__ __launch_bounds__(kScalarBlock) void k_adam_scalar(
 }
 
 // ---------------------------------------------------------------------------
-// One-launch small-shard step (cooperative launch: every workgroup of the grid
-// is resident at once, which the grid barrier below relies on).  The shard's
-// vector layout is k_adam_vec's (`head` scalar elements, `nvec` 4-element
-// vectors, a tail of 0..3); workgroup b owns vectors (b*V + u)*kSmallBlock +
-// threadIdx.x for u < V, so consecutive lanes touch consecutive vectors.
-//   1. Load the thread's gradient vectors, sum their exact squares in fp64,
-//      reduce over the workgroup (workgroup 0 also takes the head and tail
-//      elements) and store the workgroup's partial part[b].
-//   2. Arrive at the barrier (a release increment of *bar), then issue the
-//      loads of theta, m and v, which overlap the wait.
-//   3. Wait until *bar reaches bar_target (the host passes the count of
-//      arrivals this counter had received before the launch plus the grid
-//      size).  The wait is bounded: a workgroup that gives up writes nothing,
-//      and workgroup 0 then does not publish the record, so the host's wait
-//      ends with an error once the stream is idle.
-//   4. Every workgroup totals part[0, gridDim.x) in the same fixed order, so
-//      all of them hold the same bits; workgroup 0 publishes the result record
-//      (device and host-mapped, as k_finalize does).
+// One-launch small-shard step.  The grid is small enough to be resident on
+// the device at once (the host keeps it to a fraction of the co-resident
+// capacity, so a few such steps on concurrent streams also fit together), which
+// the grid barrier below relies on.  The shard's vector layout is
+// k_adam_vec's (`head` scalar elements, `nvec` 4-element vectors, a tail of
+// 0..3); workgroup b owns vectors (b*V + u)*kSmallBlock + threadIdx.x for
+// u < V, so consecutive lanes touch consecutive vectors.
+//   1. Thread 0 reads its group's wake flag (its value before this launch),
+//      then the workgroup loads its gradient vectors, sums their exact squares
+//      in fp64 (workgroup 0 also takes the head and tail elements) and stores
+//      the workgroup's partial part[b].
+//   2. Arrival, in two levels so that no address takes more than a few dozen
+//      atomic additions (one address serialises them at about 12 ns each):
+//      workgroup b counts itself in group b mod kSyncGroups; the last of a
+//      group counts the group at the top; the last group's last workgroup is
+//      the last arrival.  Counters are reset by their last arrival.
+//   3. The state loads of theta, m and v are issued (they overlap the wait).
+//   4. The last arrival claims the launch, totals part[0, gridDim.x) in a
+//      fixed order, publishes the result record (device and host-mapped),
+//      then writes every group's wake flag: a launch count in the high bits,
+//      the skip flag and the fp32 multiplier in the low 33, so a waiter reads
+//      the step's scalars from the word it polls.  The others wait for their
+//      group's flag to change.
 //   5. Unless the step is skipped, the update from the registers.
+// The wait is bounded.  A workgroup that gives up tries to claim the launch
+// as aborted; the claim word makes completion and abort exclusive, so either
+// every workgroup updates or none does (then nothing is written, the record
+// is not published and the host's wait ends with an error once the stream
+// is idle).  Partials, counters, flags and the claim word are accessed with
+// agent-scope atomic operations, which the device keeps coherent across its
+// XCDs without writing back or invalidating the L2 caches; a store completes
+// (s_waitcnt) before the operation that announces it is issued.
 // ---------------------------------------------------------------------------
 constexpr int kSmallBlock = 256;
-constexpr uint32_t kBarrierSpinLimit = 1u << 22;  // polls of about 0.1-1 us each
+constexpr int kSyncGroups = 16;
+constexpr int kSyncStride = 32;                        // words between sync words (256 bytes)
+constexpr uint32_t kBarrierSpinLimit = 1u << 22;       // polls of about 0.1-1 us each
+// Word offsets in the sync area (each word on its own 256-byte line).
+constexpr int kSyncGroupCtr = 0;                       // kSyncGroups group counters
+constexpr int kSyncTop = kSyncGroups;                  // the count of complete groups
+constexpr int kSyncFlag = kSyncGroups + 1;             // kSyncGroups wake flags
+constexpr int kSyncClaim = 2 * kSyncGroups + 1;        // 0 open, 1 completed, 2 aborted
+constexpr int kSyncWords = (2 * kSyncGroups + 2) * kSyncStride;
+constexpr uint64_t kFlagCount = (uint64_t)1 << 33;     // a wake flag's launch count unit
+
+__device__ __forceinline__ uint64_t* sync_word(uint64_t* sync, int k) { return sync + (int64_t)k * kSyncStride; }
+
+__device__ __forceinline__ uint64_t aload(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void astore(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t aadd(uint64_t* p, uint64_t v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool acas(uint64_t* p, uint64_t expect, uint64_t v) {
+    return __hip_atomic_compare_exchange_strong(p, &expect, v, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Waiter (thread 0 of a workgroup that is not the last arrival): true when its
+// group's flag has moved on from `flag0` (the launch completed; *word is the
+// new flag), false when the launch was aborted.  The last arrival writes every
+// flag before it reopens the claim word, so a flag that has not moved while the
+// claim reads "aborted" means a real abort.
+__device__ __forceinline__ bool small_wait(uint64_t* sync, int grp, uint64_t flag0, uint64_t* word) {
+    uint64_t* flag = sync_word(sync, kSyncFlag + grp);
+    uint64_t* claim = sync_word(sync, kSyncClaim);
+    const uint64_t count0 = flag0 / kFlagCount;
+    uint32_t polls = 0;
+    for (;;) {
+        if ((*word = aload(flag)) / kFlagCount != count0)
+            return true;
+        ++polls;
+        if ((polls & 1023) == 0 && aload(claim) == 2)
+            return (*word = aload(flag)) / kFlagCount != count0;
+        if (polls >= kBarrierSpinLimit) {
+            polls = 0;
+            if (acas(claim, 0, 2)) {
+                __builtin_amdgcn_s_waitcnt(0);
+                if ((*word = aload(flag)) / kFlagCount != count0) {
+                    astore(claim, 0);  // the launch had completed just before: undo the claim
+                    return true;
+                }
+                return false;
+            }
+            // claimed as completed (the flag follows) or as aborted (the check above sees it)
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
 
 template <int V>
 __global__ __launch_bounds__(kSmallBlock) void k_small_step(
     const uint16_t* __restrict__ g, float* __restrict__ th, float* __restrict__ m, float* __restrict__ v,
-    uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec, double* __restrict__ part,
-    uint64_t* __restrict__ bar, uint64_t bar_target, Result* __restrict__ res, Result* __restrict__ res_host,
-    double loss_scale, double clip, uint32_t seq, AdamConst c) {
+    uint16_t* __restrict__ p, int64_t n, int64_t head, int64_t nvec, uint64_t* __restrict__ part,
+    uint64_t* __restrict__ sync, Result* __restrict__ res, Result* __restrict__ res_host, double loss_scale,
+    double clip, uint32_t seq, AdamConst c) {
     __shared__ float s_mult;
-    __shared__ int s_skip;
+    __shared__ int s_state;  // 1: this workgroup is the last arrival; then 0 proceed, 1 skip, 2 abort
     const u32x2* __restrict__ gv = reinterpret_cast<const u32x2*>(g + head);
     f32x4* __restrict__ tv = reinterpret_cast<f32x4*>(th + head);
     f32x4* __restrict__ mv = reinterpret_cast<f32x4*>(m + head);
     f32x4* __restrict__ vv = reinterpret_cast<f32x4*>(v + head);
     u32x2* __restrict__ pv = reinterpret_cast<u32x2*>(p + head);
     const int64_t b = blockIdx.x;
+    const int G = (int)gridDim.x;
+    const int grp = (int)(b % kSyncGroups);
+    const int ngroups = G < kSyncGroups ? G : kSyncGroups;
+    uint64_t flag0 = 0;
+    if (threadIdx.x == 0)
+        flag0 = aload(sync_word(sync, kSyncFlag + grp));  // before arriving: it cannot move until then
 
     // 1. statistics of this workgroup's gradient vectors
     u32x2 gq[V];
@@ -608,11 +693,20 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_step(
     }
     const double ps = block_sum<kSmallBlock>(a0 + a1);
 
-    // 2. publish the partial and arrive; then the state loads
+    // 2. publish the partial and arrive (two levels)
     if (threadIdx.x == 0) {
-        part[b] = ps;
-        __hip_atomic_fetch_add(bar, (uint64_t)1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        astore(part + b, __builtin_bit_cast(uint64_t, ps));
+        __builtin_amdgcn_s_waitcnt(0);
+        const uint64_t gsize = (uint64_t)((G - grp + kSyncGroups - 1) / kSyncGroups);
+        uint64_t* gctr = sync_word(sync, kSyncGroupCtr + grp);
+        int last = 0;
+        if (aadd(gctr, 1) == gsize - 1) {
+            astore(gctr, 0);  // every member has counted: ready for the next launch
+            last = aadd(sync_word(sync, kSyncTop), 1) == (uint64_t)(ngroups - 1);
+        }
+        s_state = last;
     }
+    // 3. the state loads, overlapping the wait
     f32x4 tq[V], mq[V], vq[V];
 #pragma unroll
     for (int u = 0; u < V; ++u) {
@@ -623,43 +717,49 @@ __global__ __launch_bounds__(kSmallBlock) void k_small_step(
             vq[u] = ld<true>(vv + i);
         }
     }
+    __syncthreads();
 
-    // 3. bounded wait for every workgroup's arrival
-    if (threadIdx.x == 0) {
-        uint32_t polls = 0;
-        s_skip = 0;
-        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < bar_target) {
-            __builtin_amdgcn_s_sleep(1);
-            if (++polls >= kBarrierSpinLimit) {
-                s_skip = 2;  // gave up: write nothing
-                break;
+    // 4. the last arrival totals and publishes; the others wait for their flag
+    if (s_state == 1) {
+        double s0 = 0.0;
+        for (int64_t i = threadIdx.x; i < G; i += kSmallBlock)
+            s0 += __builtin_bit_cast(double, aload(part + i));
+        const double tot = block_sum<kSmallBlock>(s0);
+        if (threadIdx.x == 0) {
+            uint64_t* claim = sync_word(sync, kSyncClaim);
+            if (!acas(claim, 0, 1)) {
+                s_state = 2;  // a waiter gave up first: nobody writes
+            } else {
+                const Result r = make_result(tot, loss_scale, clip, seq);
+                *res = r;
+                Result rh = r;
+                rh.seq = 0;
+                *res_host = rh;
+                __hip_atomic_store(&res_host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+                s_mult = r.mult;
+                s_state = r.skip;
+                astore(sync_word(sync, kSyncTop), 0);
+                // every flag is written, whatever the grid, so all of them always hold the same
+                // launch count (a waiter's group flag then always changes)
+                const uint64_t word = (flag0 / kFlagCount + 1) * kFlagCount +
+                                      ((uint64_t)__builtin_bit_cast(uint32_t, r.mult) | ((uint64_t)(uint32_t)r.skip << 32));
+                for (int k = 0; k < kSyncGroups; ++k)
+                    astore(sync_word(sync, kSyncFlag + k), word);
+                __builtin_amdgcn_s_waitcnt(0);
+                astore(claim, 0);  // after the flags: see small_wait
             }
         }
-    }
-    __syncthreads();
-    if (s_skip == 2)
-        return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other workgroups' partials are visible
-
-    // 4. the total, in the same fixed order in every workgroup
-    double s0 = 0.0;
-    for (int64_t i = threadIdx.x; i < (int64_t)gridDim.x; i += kSmallBlock)
-        s0 += part[i];
-    const double tot = block_sum<kSmallBlock>(s0);
-    if (threadIdx.x == 0) {
-        const Result r = make_result(tot, loss_scale, clip, seq);
-        s_mult = r.mult;
-        s_skip = r.skip;
-        if (b == 0) {
-            *res = r;
-            Result rh = r;
-            rh.seq = 0;
-            *res_host = rh;
-            __hip_atomic_store(&res_host->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    } else if (threadIdx.x == 0) {
+        uint64_t w = 0;
+        if (!small_wait(sync, grp, flag0, &w)) {
+            s_state = 2;
+        } else {
+            s_mult = __builtin_bit_cast(float, (uint32_t)w);
+            s_state = (int)((w >> 32) & 1);
         }
     }
     __syncthreads();
-    if (s_skip)
+    if (s_state)
         return;
     const float mult = s_mult;
 

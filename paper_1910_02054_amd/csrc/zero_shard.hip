@@ -68,10 +68,18 @@ constexpr bool kCopyNTL = true, kCopyNTS = true, kCopyXCD = false;
 constexpr int64_t kSmallMaxNumel = ZS_SMALL_MAX_NUMEL;
 constexpr int64_t kSmallMaxGrid = 512;
 // A grid takes at most 1/kSmallCapShare of the device's co-resident capacity,
-// so the barrier-waiting workgroups of cooperative steps running at once on
-// several streams (the hardware queues a process gets) always fit together.
-constexpr int64_t kSmallCapShare = 8;
+// so the barrier-waiting workgroups of small steps running at once on several
+// streams (one per hardware queue; HIP gives a process four by default) always
+// fit on the device together.
+#ifndef ZS_SMALL_CAP_SHARE
+#define ZS_SMALL_CAP_SHARE 4
+#endif
+constexpr int64_t kSmallCapShare = ZS_SMALL_CAP_SHARE;
 constexpr int kSmallV[4] = {1, 2, 4, 8};
+#ifndef ZS_SMALL_FIRST_V
+#define ZS_SMALL_FIRST_V 0
+#endif
+constexpr int kSmallFirstV = ZS_SMALL_FIRST_V;  // index into kSmallV of the first variant tried
 
 // ---------------------------------------------------------------------------
 // Launch planning.  One function decides every launch shape from n and the
@@ -129,7 +137,7 @@ void plan_small(Plan* pl, int64_t n, const DevInfo* info) {
     pl->small_grid = 0;
     if (!pl->vec || n > kSmallMaxNumel)
         return;
-    for (int k = 0; k < 4; ++k) {
+    for (int k = kSmallFirstV; k < 4; ++k) {
         int64_t grid = ceil_div(pl->nvec, (int64_t)zs::kSmallBlock * kSmallV[k]);
         if (grid < 1)
             grid = 1;
@@ -206,12 +214,7 @@ int dev_info(int dev, const DevInfo** out) {
                 reinterpret_cast<const void*>(
                     zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>),
                 kAdamBlock, kAdamPerCU, prop, &d.adam_resident);
-            int coop = 0;
-            if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess) {
-                (void)hipGetLastError();
-                coop = 0;
-            }
-            for (int k = 0; k < 4 && coop; ++k) {
+            for (int k = 0; k < 4; ++k) {
                 int per_cu = 0;
                 if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, small_kernel(kSmallV[k]), zs::kSmallBlock,
                                                                  0) != hipSuccess) {
@@ -238,11 +241,11 @@ std::map<std::pair<int, hipStream_t>, std::shared_ptr<Ctx>> g_ctx;
 void free_ctx_buffers(Ctx* c) {
     if (c->part) (void)hipFree(c->part);
     if (c->res) (void)hipFree(c->res);
-    if (c->bar) (void)hipFree(c->bar);
+    if (c->sync) (void)hipFree(c->sync);
     if (c->host) (void)hipHostFree(c->host);
     c->part = nullptr;
     c->res = nullptr;
-    c->bar = nullptr;
+    c->sync = nullptr;
     c->host = c->host_dev = nullptr;
 }
 
@@ -272,10 +275,10 @@ int new_ctx(int dev, hipStream_t stream, const DevInfo* info, std::shared_ptr<Ct
     c->stream = stream;
     c->info = info;
     RelaxedCapture relaxed(stream);
-    // the barrier counter is zeroed on the stream before the first small-shard launch
+    // the barrier words are zeroed on the stream before the first small-shard launch
     bool ok = hipMalloc(reinterpret_cast<void**>(&c->part), sizeof(zs::Partial) * zs::kMaxStatsBlocks) == hipSuccess &&
               hipMalloc(reinterpret_cast<void**>(&c->res), sizeof(zs::Result)) == hipSuccess &&
-              hipMalloc(reinterpret_cast<void**>(&c->bar), sizeof(uint64_t)) == hipSuccess &&
+              hipMalloc(reinterpret_cast<void**>(&c->sync), sizeof(uint64_t) * zs::kSyncWords) == hipSuccess &&
               hipHostMalloc(reinterpret_cast<void**>(&c->host), sizeof(zs::Result),
                             hipHostMallocMapped | hipHostMallocCoherent) == hipSuccess &&
               hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_dev), c->host, 0) == hipSuccess;
@@ -626,31 +629,32 @@ int launch_update(Ctx* ctx, const uint16_t* grad16, float* master32, float* m32,
 }
 
 // The one-launch small-shard step (pl.small_v > 0) with its partials in `part`
-// and its barrier counter at `bar`, whose arrivals so far are *bar_count
-// (advanced by the grid when the launch is accepted).
-int launch_small_into(double* part, uint64_t* bar, uint64_t* bar_count, bool* bar_ready, zs::Result* res,
-                      zs::Result* host_dev, const uint16_t* grad16, float* master32, float* m32, float* v32,
-                      uint16_t* param16_out, int64_t n, const Plan& pl, double loss_scale, double clip, uint32_t seq,
-                      const zs::AdamConst& c, hipStream_t stream) {
-    if (!*bar_ready) {
-        zs::k_set_u64<<<1, 64, 0, stream>>>(bar, 0);
+// and its barrier words at `sync` (zeroed on the stream first when
+// *sync_ready is false).
+int launch_small_into(uint64_t* part, uint64_t* sync, bool* sync_ready, zs::Result* res, zs::Result* host_dev,
+                      const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                      int64_t n, const Plan& pl, double loss_scale, double clip, uint32_t seq, const zs::AdamConst& c,
+                      hipStream_t stream) {
+    if (!*sync_ready) {
+        zs::k_zero_words<<<1, 256, 0, stream>>>(sync, zs::kSyncWords);
         HIP_TRY(hipGetLastError());
-        *bar_count = 0;
-        *bar_ready = true;
+        *sync_ready = true;
     }
-    const uint64_t target = *bar_count + (uint64_t)pl.small_grid;
-    int64_t head = pl.head, nvec = pl.nvec;
-    void* args[] = {&grad16, &master32, &m32, &v32, &param16_out, &n, &head, &nvec, &part, &bar,
-                    const_cast<uint64_t*>(&target), &res, &host_dev, &loss_scale, &clip, &seq,
-                    const_cast<zs::AdamConst*>(&c)};
-    const hipError_t e = hipLaunchCooperativeKernel(small_kernel(pl.small_v), dim3((unsigned)pl.small_grid),
-                                                    dim3(zs::kSmallBlock), args, 0, stream);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return fail(ZERO_EHIP, "cooperative launch of the small-shard step (%lld workgroups): %s",
-                    (long long)pl.small_grid, hipGetErrorString(e));
+    const dim3 grid((unsigned)pl.small_grid), block(zs::kSmallBlock);
+#define ZS_SMALL_LAUNCH(V)                                                                                      \
+    zs::k_small_step<V><<<grid, block, 0, stream>>>(grad16, master32, m32, v32, param16_out, n, pl.head, pl.nvec, \
+                                                    part, sync, res, host_dev, loss_scale, clip, seq, c)
+    switch (pl.small_v) {
+    case 1: ZS_SMALL_LAUNCH(1); break;
+    case 2: ZS_SMALL_LAUNCH(2); break;
+    case 4: ZS_SMALL_LAUNCH(4); break;
+    default: ZS_SMALL_LAUNCH(8); break;
     }
-    *bar_count = target;
+#undef ZS_SMALL_LAUNCH
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return fail(ZERO_EHIP, "launch of the small-shard step (%lld workgroups): %s", (long long)pl.small_grid,
+                    hipGetErrorString(e));
     return ZERO_OK;
 }
 
@@ -892,9 +896,9 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
         // one launch: its whole time counts as the update's
         if (prof)
             prof_record(pr.mid, stream, &pr);
-        rc = launch_small_into(reinterpret_cast<double*>(ctx->part), ctx->bar, &ctx->bar_count, &ctx->bar_ready,
-                               ctx->res, ctx->host_dev, grad16, master32, m32, v32, param16_out, n, pl, loss_scale,
-                               clip, seq, c, stream);
+        rc = launch_small_into(reinterpret_cast<uint64_t*>(ctx->part), ctx->sync, &ctx->sync_ready, ctx->res,
+                               ctx->host_dev, grad16, master32, m32, v32, param16_out, n, pl, loss_scale, clip, seq,
+                               c, stream);
     } else {
         rc = launch_stats_into(ctx->info, ctx->part, ctx->res, ctx->host_dev, grad16, n, pl, loss_scale, clip, seq,
                                stream);
@@ -916,8 +920,11 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
     }
     // The update is already queued: wait only for the statistics.
     zs::Result r;
-    if ((rc = wait_result(ctx.get(), seq, stream, &r)))
+    if ((rc = wait_result(ctx.get(), seq, stream, &r))) {
+        if (pl.small_v)
+            ctx->sync_ready = false;  // an aborted launch's barrier words are cleared before the next
         return rc;
+    }
     set_stats(r, n, pl.small_v ? 1 : 0);
     return r.skip ? ZERO_SKIPPED : ZERO_OK;
 }
