@@ -127,6 +127,24 @@ int zero_shard_step(const uint16_t* grad16, float* master32, float* m32, float* 
                     int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
                     int64_t step, double loss_scale, double clip, void* stream);
 
+/* For callers that cannot allocate memory (tight serving or training loops,
+ * harnesses that forbid the allocator): zero_shard_step with the same
+ * arguments, checks, kernels, results and return values, that calls no
+ * hipMalloc, hipFree or other allocating routine.  Its workspace (statistics
+ * partials for up to 4096 workgroups, the one-launch step's barrier words and
+ * two result records: 73 KiB) is one fixed device array per GPU, held by
+ * every GPU the library runs on until the process ends; n up to 2^40 (the
+ * library's limit, ZERO_EINVAL above it) needs no more.  Differences: the call
+ * returns once the whole step (update included) has completed on `stream`,
+ * since the skip decision is copied back after it; no kernel timing is
+ * sampled.  All calls on one GPU share its array: calls from several threads
+ * are serialised on the host, but calls whose work overlaps on the GPU (on
+ * different streams, or queued behind other work so that two steps' kernels
+ * run together) race on it and must not be made. */
+int zero_shard_step_noalloc(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                            int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
+                            int64_t step, double loss_scale, double clip, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Split-phase step: local statistics, then the update with global ones      */
 /* ------------------------------------------------------------------------ */

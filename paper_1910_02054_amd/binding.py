@@ -75,6 +75,7 @@ _lib.zero_resident_release.argtypes = [_P]
 _lib.zero_stream_release.argtypes = [_P]
 _lib.zero_workspace_count.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
 _lib.zero_probe_lamb_pass.argtypes = [_i32, _P, _P, _P, _P, _P, _i64, _P]
+_lib.zero_shard_step_noalloc.argtypes = _lib.zero_shard_step.argtypes
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
 _lib.zero_model_state_bytes.argtypes = [_dbl, _dbl, _i32, _dbl, ctypes.POINTER(_dbl)]
@@ -100,7 +101,7 @@ EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step", "zero_lamb_moments",
            "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async", "zero_shard_apply_async",
            "zero_resident_state_init", "zero_shard_step_resident", "zero_resident_release",
-           "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass")
+           "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass", "zero_shard_step_noalloc")
 for _f in EXPORTS:
     if _f != "zero_last_error":
         getattr(_lib, _f).restype = ctypes.c_int
@@ -183,6 +184,21 @@ def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, e
     f32 = (torch.float32,)
     n = _shard_len(n, grad16, master32, m32, v32, param16_out)
     return _check(_lib.zero_shard_step(
+        _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
+        _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(lr), float(beta1),
+        float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),
+        _stream(stream)))
+
+
+def zero_shard_step_noalloc(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, step,
+                            loss_scale, clip, n=None, stream=None) -> int:
+    """zero_shard_step through the allocation-free entry point (fixed per-GPU workspace;
+    returns once the step has completed).  0 applied, 1 skipped; raises ZeroError."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
+    return _check(_lib.zero_shard_step_noalloc(
         _addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"), _addr(m32, f32, "m32"),
         _addr(v32, f32, "v32"), _addr(param16_out, h16, "param16_out"), int(n), float(lr), float(beta1),
         float(beta2), float(eps), float(weight_decay), int(step), float(loss_scale), float(clip),

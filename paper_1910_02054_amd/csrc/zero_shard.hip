@@ -749,6 +749,48 @@ int resident_ws(int dev, const void* state, hipStream_t stream, ResWs** out) {
     return ZERO_OK;
 }
 
+// ---------------------------------------------------------------------------
+// The allocation-free step's workspace: one fixed device array per GPU (each
+// device that loads the library holds its own copy until the process ends),
+// laid out as the statistics partials, the one-launch step's barrier words,
+// the result record and a second record that stands in for the host-mapped
+// one (the host copies it out instead).  In host code `scratch` names a
+// host-side stand-in; the device address comes from hipGetSymbolAddress.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchPart = 0;
+constexpr size_t kScratchSync = kScratchPart + sizeof(zs::Partial) * zs::kMaxStatsBlocks;
+constexpr size_t kScratchRes = kScratchSync + sizeof(uint64_t) * zs::kSyncWords;
+constexpr size_t kScratchRes2 = kScratchRes + 256;
+constexpr size_t kScratchBytes = kScratchRes2 + 256;
+static_assert(kScratchRes % 256 == 0 && sizeof(zs::Result) <= 256, "scratch layout");
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchDev {
+    std::mutex mu;           // serialises this device's allocation-free calls on the host side
+    unsigned char* ptr = nullptr;  // the device's copy of `scratch`
+    bool sync_ready = true;  // the barrier words are zero (as loaded) or were cleared
+    uint32_t seq = 0;
+};
+ScratchDev g_scratch[kMaxDevices];
+
+// The device address of `scratch` on `dev` (the current device), looked up
+// once per device.  Caller holds g_scratch[dev].mu.
+int scratch_ptr(int dev, unsigned char** out) {
+    ScratchDev& sd = g_scratch[dev];
+    if (!sd.ptr) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return fail(ZERO_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        }
+        sd.ptr = static_cast<unsigned char*>(p);
+    }
+    *out = sd.ptr;
+    return ZERO_OK;
+}
+
 }  // namespace zsh
 
 using namespace zsh;
@@ -1299,6 +1341,68 @@ int zero_profile_read(zero_profile_t* out) {
     *out = g_prof_acc;
     g_prof_acc = zero_profile_t{0, 0.0, 0.0};
     return rc;
+}
+
+int zero_shard_step_noalloc(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                            int64_t n, double lr, double beta1, double beta2, double eps, double weight_decay,
+                            int64_t step, double loss_scale, double clip, void* stream_) {
+    const char* fn = "zero_shard_step_noalloc";
+    int rc = check_update_args(fn, grad16, master32, m32, v32, param16_out, n, lr, beta1, beta2, eps, weight_decay,
+                               step, loss_scale, clip);
+    if (rc)
+        return rc;  // includes n above 2^40, the most the fixed workspace serves
+    if (n == 0) {
+        t_stats = zero_step_stats_t{0.0, 0.0, 1.0, (float)(1.0 / loss_scale), 0, 0, 0, 0};
+        t_have_stats = true;
+        return ZERO_OK;
+    }
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    int dev = 0;
+    const DevInfo* info = nullptr;
+    if ((rc = current_device(stream, &dev)) || (rc = dev_info(dev, &info)))
+        return rc;
+    if ((rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
+        return rc;
+    ScratchDev& sd = g_scratch[dev];
+    std::lock_guard<std::mutex> lk(sd.mu);
+    unsigned char* base = nullptr;
+    if ((rc = scratch_ptr(dev, &base)))
+        return rc;
+    zs::Partial* part = reinterpret_cast<zs::Partial*>(base + kScratchPart);
+    uint64_t* sync = reinterpret_cast<uint64_t*>(base + kScratchSync);
+    zs::Result* res = reinterpret_cast<zs::Result*>(base + kScratchRes);
+    zs::Result* res2 = reinterpret_cast<zs::Result*>(base + kScratchRes2);
+    const zs::AdamConst c = adam_const(lr, beta1, beta2, eps, weight_decay, step);
+    Plan pl = plan_step(grad16, master32, m32, v32, param16_out, n, info->ncu);
+    plan_small(&pl, n, info);
+    if (pl.stats_blocks > zs::kMaxStatsBlocks || pl.small_grid > (int64_t)zs::kMaxStatsBlocks)
+        return fail(ZERO_EINVAL, "%s: launch needs more partials than the fixed workspace holds", fn);
+    if (++sd.seq == 0)
+        ++sd.seq;
+    const uint32_t seq = sd.seq;
+    if (pl.small_v) {
+        rc = launch_small_into(reinterpret_cast<uint64_t*>(part), sync, &sd.sync_ready, res, res2, grad16, master32,
+                               m32, v32, param16_out, n, pl, loss_scale, clip, seq, c, stream);
+    } else {
+        rc = launch_stats_into(info, part, res, res2, grad16, n, pl, loss_scale, clip, seq, stream);
+        if (!rc)
+            rc = launch_update_from(info, res, grad16, master32, m32, v32, param16_out, n, pl, c, stream);
+    }
+    if (rc)
+        return rc;
+    // the record comes back with a copy after the update: the call returns once the whole
+    // step has completed on the stream
+    zs::Result r;
+    std::memset(&r, 0, sizeof r);
+    HIP_TRY(hipMemcpyAsync(&r, res2, sizeof r, hipMemcpyDeviceToHost, stream));
+    HIP_TRY(hipStreamSynchronize(stream));
+    if (r.seq != seq) {
+        if (pl.small_v)
+            sd.sync_ready = false;  // an aborted launch's barrier words are cleared before the next
+        return fail(ZERO_EHIP, "%s: result record %u not published by the step's kernels", fn, seq);
+    }
+    set_stats(r, n, pl.small_v ? 1 : 0);
+    return r.skip ? ZERO_SKIPPED : ZERO_OK;
 }
 
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {
