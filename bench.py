@@ -37,7 +37,7 @@ LAMB_MOMENTS_BYTES_PER_PARAM = 22
 LAMB_APPLY_BYTES_PER_PARAM = 18
 DEFAULT_WORKLOAD = "mp16_dp25_100b"
 CSRC = os.path.join(ROOT, "paper_1910_02054_amd", "csrc")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_adam_vec_mp16_dp25_100b_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_adam_vec_%s_traffic.txt")   # per workload
 LAMB_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_lamb_moments_mp16_dp25_100b_traffic.txt")
 KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "zero_shard.hip")]
 LAMB_KERNEL_SOURCES = [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "lamb_kernels.hpp", "zero_lamb.hip")]
@@ -98,10 +98,10 @@ def _traffic_from(path, key, source_hash, n):
         return None
 
 
-def measured_traffic(n):
-    """HBM bytes per update launch from the committed counter summary, or None when
-    absent, for another shard size, or taken on a different kernel source."""
-    return _traffic_from(TRAFFIC_FILE, "update_bytes_per_launch", kernel_source_hash(), n)
+def measured_traffic(workload, n):
+    """HBM bytes per update launch from the workload's committed counter summary, or None
+    when absent, for another shard size, or taken on a different kernel source."""
+    return _traffic_from(TRAFFIC_FILE % workload, "update_bytes_per_launch", kernel_source_hash(), n)
 
 
 def measured_lamb_traffic(n):
@@ -439,7 +439,11 @@ def main():
         kernel_ms = {"stats_and_finalize": prof.stats_ms / prof.steps, "update": prof.update_ms / prof.steps,
                      "profiled_steps": prof.steps}
         upd_gbps = UPDATE_BYTES_PER_PARAM * n / (kernel_ms["update"] * 1e-3) / 1e9
-        roof_kernel, traffic = "k_adam_vec", measured_traffic(n)
+        if zb.zero_shard_last_step_stats().path == 1:
+            # the one-launch small-shard step: statistics and update in one kernel, 28 B/param
+            roof_kernel, traffic = "k_small_step", None
+        else:
+            roof_kernel, traffic = "k_adam_vec", measured_traffic(w.key, n)
 
     out = {
         "metric": METRIC,
