@@ -111,7 +111,8 @@ int zero_partition_layout(int64_t total_numel, int32_t nd, int32_t rank, zero_la
  * buffer each on its own 2 MiB boundary, run fastest; arrays offset from one
  * another by a few hundred bytes run about 5 % slower.  Shards small enough
  * for one resident grid (a quarter of the device's co-resident capacity for
- * the kernel: about 1.5 million elements on MI355X) whose arrays share one
+ * the kernel, or 1/q with q = GPU_MAX_HW_QUEUES when that is larger: about
+ * 1.5 million elements on MI355X with the default four queues) whose arrays share one
  * misalignment take a single launch (statistics, a grid barrier and the
  * update in one kernel, the gradient read once); larger ones take the
  * statistics kernels and the update kernel.  The barrier relies on the whole

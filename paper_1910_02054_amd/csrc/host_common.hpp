@@ -42,6 +42,7 @@ struct DevInfo {
     size_t stats_lds = 0, adam_lds = 0;
     int stats_resident = 0, adam_resident = 0;
     int64_t small_cap[4] = {};  // co-resident workgroups of k_small_step<1, 2, 4, 8>
+    int64_t small_share = 4;    // a one-launch grid takes at most small_cap / small_share
 };
 
 // The facts of device `dev` (0 <= dev < kMaxDevices), filled on first use.

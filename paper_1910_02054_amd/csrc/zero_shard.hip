@@ -10,6 +10,7 @@
 
 #include <cmath>
 #include <cstdarg>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <algorithm>
@@ -67,14 +68,25 @@ constexpr bool kCopyNTL = true, kCopyNTS = true, kCopyXCD = false;
 #endif
 constexpr int64_t kSmallMaxNumel = ZS_SMALL_MAX_NUMEL;
 constexpr int64_t kSmallMaxGrid = 512;
-// A grid takes at most 1/kSmallCapShare of the device's co-resident capacity,
-// so the barrier-waiting workgroups of small steps running at once on several
-// streams (one per hardware queue; HIP gives a process four by default) always
-// fit on the device together.
+// A grid takes at most 1/share of the device's co-resident capacity, where
+// share is the number of hardware queues the process may use (at least
+// kSmallCapShare; HIP gives a process four unless GPU_MAX_HW_QUEUES says
+// otherwise), so the barrier-waiting workgroups of small steps running at once
+// on every queue always fit on the device together.
 #ifndef ZS_SMALL_CAP_SHARE
 #define ZS_SMALL_CAP_SHARE 4
 #endif
 constexpr int64_t kSmallCapShare = ZS_SMALL_CAP_SHARE;
+
+int64_t small_cap_share() {
+    int64_t share = kSmallCapShare;
+    if (const char* e = std::getenv("GPU_MAX_HW_QUEUES")) {
+        const long q = std::strtol(e, nullptr, 10);
+        if (q > share)
+            share = q;
+    }
+    return share;
+}
 constexpr int kSmallV[4] = {1, 2, 4, 8};
 #ifndef ZS_SMALL_FIRST_V
 #define ZS_SMALL_FIRST_V 0
@@ -141,7 +153,7 @@ void plan_small(Plan* pl, int64_t n, const DevInfo* info) {
         int64_t grid = ceil_div(pl->nvec, (int64_t)zs::kSmallBlock * kSmallV[k]);
         if (grid < 1)
             grid = 1;
-        if (grid <= kSmallMaxGrid && grid <= info->small_cap[k] / kSmallCapShare) {
+        if (grid <= kSmallMaxGrid && grid <= info->small_cap[k] / info->small_share) {
             pl->small_v = kSmallV[k];
             pl->small_grid = grid;
             return;
@@ -223,6 +235,7 @@ int dev_info(int dev, const DevInfo** out) {
                 }
                 d.small_cap[k] = (int64_t)per_cu * d.ncu;
             }
+            d.small_share = small_cap_share();
             g_dev[dev] = d;
             g_dev_ready[dev].store(true, std::memory_order_release);
         }
