@@ -310,6 +310,11 @@ def main():
             graphs.append(gr)
         torch.cuda.synchronize()
 
+    # the fused step through the binding's prepared call (arrays and stream resolved once; the
+    # library still checks every array on every call)
+    prepared = zb.ShardStepCall(d_gs, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
+                                w.clip, stream=stream)
+
     def step():
         d_g = d_gs[scaler.t_next % 2]
         if args.resident == "graph":
@@ -339,8 +344,8 @@ def main():
             flag = zb.zero_lamb_step(plan, d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps,
                                      w.weight_decay, scaler.t_next, scaler.scale, w.clip, stream=stream)
         else:
-            flag = zb.zero_shard_step(d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
-                                      scaler.t_next, scaler.scale, w.clip, stream=stream)
+            t = scaler.t_next
+            flag = prepared(t, scaler.scale, t % 2)
         scaler.update(flag)
         return flag
 

@@ -190,6 +190,41 @@ def zero_shard_step(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, e
         _stream(stream)))
 
 
+class ShardStepCall:
+    """zero_shard_step with its arrays, fixed hyperparameters and stream resolved once.
+
+    For loops that step the same buffers many times (the gradient buffer refilled by the
+    reduce-scatter, or one of a few such buffers): the tensors are checked here as
+    zero_shard_step checks them, referenced for the object's lifetime (their storage must not
+    be resized or swapped meanwhile), and each call passes only t, the loss scale and which
+    gradient buffer to use.  The library still checks every array's allocation on every call.
+    `stream` is taken now (None: torch's current stream at construction)."""
+
+    def __init__(self, grads, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, clip,
+                 stream=None):
+        import torch
+        h16, f32 = (torch.float16, torch.int16), (torch.float32,)
+        grads = list(grads)
+        if not grads:
+            raise ValueError("at least one gradient buffer is needed")
+        n = _shard_len(None, *grads, master32, m32, v32, param16_out)
+        self._keep = (grads, master32, m32, v32, param16_out)
+        self._grads = [ctypes.c_void_p(_addr(g, h16, "grad16")) for g in grads]
+        self._rest = (ctypes.c_void_p(_addr(master32, f32, "master32")), ctypes.c_void_p(_addr(m32, f32, "m32")),
+                      ctypes.c_void_p(_addr(v32, f32, "v32")), ctypes.c_void_p(_addr(param16_out, h16, "param16_out")),
+                      ctypes.c_int64(n), _dbl(float(lr)), _dbl(float(beta1)), _dbl(float(beta2)), _dbl(float(eps)),
+                      _dbl(float(weight_decay)))
+        self._clip = _dbl(float(clip))
+        self._stream = ctypes.c_void_p(_stream(stream))
+        self._fn = _lib.zero_shard_step
+        self.n = n
+
+    def __call__(self, step, loss_scale, which=0) -> int:
+        """One step with t = step on gradient buffer `which`: 0 applied, 1 skipped."""
+        rc = self._fn(self._grads[which], *self._rest, step, loss_scale, self._clip, self._stream)
+        return _check(rc) if rc < 0 else rc
+
+
 def zero_shard_step_noalloc(grad16, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, step,
                             loss_scale, clip, n=None, stream=None) -> int:
     """zero_shard_step through the allocation-free entry point (fixed per-GPU workspace;

@@ -115,3 +115,15 @@ def test_explicit_n_may_not_exceed_the_tensors(zb):
         zb.zero_shard_step(0x1000, th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1.0, 1.0)
     with pytest.raises(ValueError, match="exceeds a buffer"):
         zb.zero_probe_copy(torch.zeros(4), torch.zeros(8), 32)
+
+
+def test_prepared_step_refuses_what_the_step_refuses(zb):
+    g, th, m, v, p = _cpu_shard(8)
+    with pytest.raises(TypeError, match="device tensor"):
+        zb.ShardStepCall([g], th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1.0)
+    with pytest.raises(ValueError, match="at least one"):
+        zb.ShardStepCall([], th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1.0)
+    with pytest.raises(ValueError, match="differ in length"):
+        zb.ShardStepCall([g, torch.zeros(9, dtype=torch.float16)], th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1.0)
+    with pytest.raises(TypeError, match="grad16: dtype"):
+        zb.ShardStepCall([g.float()], th, m, v, p, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1.0)

@@ -1,7 +1,8 @@
 """bench.py's output line on the GPU: one JSON object with the contract's fields, the roofline
 entry of the dominant kernel and the oracle's CPU baseline, for the Adam and the LAMB step.
-Runs the small 1M-element shard (the counter summary, taken on the 250M shard, then does not
-apply, so `traffic` is null) with short timed regions."""
+Runs the small 1M-element shard with short timed regions: the Adam step there is the one-launch
+small-shard kernel (no counter summary is kept for it, so `traffic` is null), the LAMB step's
+dominant kernel its moments pass (its summary is for the 250M shard)."""
 import json
 import os
 import subprocess
@@ -46,7 +47,7 @@ def _check(d, kernel):
 
 def test_adam_line():
     d = _run()
-    _check(d, "k_adam_vec")
+    _check(d, "k_small_step")
     cp = d["cpu_baseline_parallel"]
     assert cp["kind"] == "oracle" and cp["cores"] >= 1 and cp["value"] > 0 and cp["unit"] == "params/s"
 

@@ -272,3 +272,31 @@ def test_alternating_grid_sizes_on_one_stream(env):
     for n, (bufs, _, ref, _) in cases.items():
         H.compare_state([b.download() for b in bufs[1:]], ref)
         assert all(b.guards_intact() for b in bufs)
+
+
+def test_prepared_step_call_equals_the_step(env):
+    # the binding's prepared call (arrays and stream resolved once) runs the same C entry point:
+    # bitwise the step's results, with two gradient buffers in turn and an overflow on the way
+    torch, zb, dev = env
+    n = 262_147
+    _, theta, m, v = workloads.random_case(5600, n)
+    grads = [workloads.random_case(5601 + k, n)[0] for k in range(2)]
+    grads[1][n // 3] = 0x7E00   # the second buffer overflows
+    a, b = _alloc(torch, dev, n), _alloc(torch, dev, n)
+    for bufs in (a, b):
+        for buf, arr in zip(bufs[1:], (theta, m, v, workloads.p16_sentinel(n))):
+            buf.upload(arr)
+    dg = [torch.from_numpy(g.view(np.int16)).to(dev).view(torch.float16) for g in grads]
+    call = zb.ShardStepCall(dg, *(x.view for x in a[1:]), HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], 0.0, 1.0)
+    t = 1
+    for k in range(6):
+        which = 1 if k == 3 else 0
+        f1 = call(t, 2.0 ** 16, which)
+        f2 = zb.zero_shard_step(dg[which], *(x.view for x in b[1:]), HP["lr"], HP["beta1"], HP["beta2"], HP["eps"],
+                                0.0, t, 2.0 ** 16, 1.0)
+        assert f1 == f2 == (1 if which else 0)
+        t += 1 - f1
+    torch.cuda.synchronize()
+    for x, y in zip(a[1:], b[1:]):
+        assert np.array_equal(x.download().view(np.uint8), y.download().view(np.uint8))
+    assert all(buf.guards_intact() for buf in a + b)
