@@ -444,7 +444,8 @@ def main():
         kernel_ms = {"stats_and_finalize": prof.stats_ms / prof.steps, "update": prof.update_ms / prof.steps,
                      "profiled_steps": prof.steps}
         upd_gbps = UPDATE_BYTES_PER_PARAM * n / (kernel_ms["update"] * 1e-3) / 1e9
-        if zb.zero_shard_last_step_stats().path == 1:
+        fused = not (args.resident or args.split_phase)
+        if fused and zb.zero_shard_last_step_stats().path == 1:
             # the one-launch small-shard step: statistics and update in one kernel, 28 B/param
             roof_kernel, traffic = "k_small_step", None
         else:

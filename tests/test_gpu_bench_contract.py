@@ -56,3 +56,13 @@ def test_lamb_line():
     d = _run("--optimizer", "lamb")
     _check(d, "k_lamb_moments")
     assert d["config"]["optimizer"] == "lamb" and d["lamb_apply"]["kernel"] == "k_lamb_apply"
+
+
+@pytest.mark.parametrize("mode", [("--resident", "eager"), ("--resident", "graph"), ("--split-phase",),
+                                  ("--split-phase", "--async-seam")])
+def test_other_step_forms_print_their_line(mode):
+    # the resident step (eager and graph replays) and the split phase (host or device seam):
+    # three kernels per step, the update's roofline entry
+    d = _run(*mode)
+    _check(d, "k_adam_vec")
+    assert "path" in d["config"]
