@@ -257,7 +257,9 @@ int zero_shard_step_resident(const uint16_t* grad16, float* master32, float* m32
 
 /* Frees the workspace the resident step holds for `state` on the current
  * device (nothing to do if it holds none).  Graph replays may use it on any
- * stream, so this first waits for the device to finish its queued work.  A
+ * stream, so this first waits for the device to finish its queued work
+ * (hipDeviceSynchronize): call it while no stream of the device is being
+ * captured, since such a wait ends a capture in progress with an error.  A
  * later step with the record allocates a new workspace; graphs captured with
  * it must not be replayed after the release.  Returns 0 or ZERO_EHIP. */
 int zero_resident_release(const zero_resident_state_t* state);
