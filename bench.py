@@ -229,6 +229,8 @@ def main():
     ap.add_argument("--resident", choices=("eager", "graph"), default=None,
                     help="adam only: the resident step (state record and loss scaler on the device, no host "
                          "wait), called eagerly or replayed from a captured HIP graph")
+    ap.add_argument("--no-adam-probe", dest="adam_probe", action="store_false",
+                    help="adam: skip the update's byte-mix probe (run after the timed steps)")
     ap.add_argument("--no-lamb-probes", dest="lamb_probes", action="store_false",
                     help="lamb only: skip the byte-mix probes of the two passes (run after the timed steps)")
     ap.add_argument("--async-seam", action="store_true",
@@ -490,6 +492,32 @@ def main():
     if probe:
         probe["update_frac_of_copy"] = upd_gbps / probe["gbps"]
         out["copy_probe"] = probe
+    if not lamb and roof_kernel == "k_adam_vec" and args.adam_probe:
+        # the update's byte mix (28 B/param) at its launch shape with trivial arithmetic, in the update's
+        # place: each probe launch follows a statistics pass over the gradient, as the update does in
+        # a step (so it finds the same part of the gradient in the cache), and is timed alone between
+        # two events on the stream, as the profiled updates are.  Runs after every timed step: the
+        # probe overwrites the state.
+        print("[bench] adam byte-mix probe", file=sys.stderr, flush=True)
+        arrs = (d_gs[0], d_theta, d_m, d_v, d_p)
+        sums = torch.zeros(1, dtype=torch.float64, device=dev)
+        for _ in range(3):
+            zb.zero_shard_stats_async(d_gs[0], sums, stream=stream)
+            zb.zero_probe_adam_mix(*arrs, stream=stream)
+        marks = []
+        for _ in range(20):
+            zb.zero_shard_stats_async(d_gs[0], sums, stream=stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            zb.zero_probe_adam_mix(*arrs, stream=stream)
+            e1.record(stream)
+            marks.append((e0, e1))
+        torch.cuda.synchronize()
+        pms = sum(a.elapsed_time(b) for a, b in marks) / len(marks)
+        pg = UPDATE_BYTES_PER_PARAM * n / (pms * 1e-3) / 1e9
+        out["adam_probe"] = {"kernel": "k_probe_adam", "probe_ms": pms, "probe_gbps": pg, "update_gbps": upd_gbps,
+                             "update_frac_of_probe": upd_gbps / pg,
+                             "context": "each launch after a statistics pass over the gradient"}
     if lamb and args.lamb_probes:
         # the byte mixes of the two LAMB passes at their launch shape with trivial arithmetic
         # (after every timed step: the probes overwrite the state), timed with events on the stream

@@ -493,6 +493,18 @@ int zero_workspace_count(int64_t* streams, int64_t* records);
  * one GPU-accessible allocation; ZERO_EINVAL otherwise, before any launch. */
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
+/* Byte-mix probe of the Adam update: one launch over the shard's arrays with
+ * the launch shape, tile walk, vector width and cache policy of the update
+ * kernel, reading grad16, master32, m32, v32 and writing master32, m32, v32,
+ * param16_out (28 bytes per element, as the update) with three adds and a
+ * conversion per element instead of Adam: the achievable time of the
+ * update's streams on this device.  The arrays it writes get meaningless
+ * values.  fp32 arrays 16-byte aligned, fp16 arrays 8-byte aligned, each
+ * inside one GPU allocation, no overlaps, 0 <= n <= 2^40; ZERO_EINVAL
+ * otherwise, before any launch.  Enqueues only. */
+int zero_probe_adam_mix(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                        int64_t n, void* stream);
+
 /* Byte-mix probes of the LAMB passes: one launch over the shard's arrays with
  * the launch shape, tile walk, vector width and cache policy of
  * k_lamb_moments (pass 0: reads grad16, master32, m32, v32; writes m32, v32)

@@ -75,6 +75,7 @@ _lib.zero_resident_release.argtypes = [_P]
 _lib.zero_stream_release.argtypes = [_P]
 _lib.zero_workspace_count.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
 _lib.zero_probe_lamb_pass.argtypes = [_i32, _P, _P, _P, _P, _P, _i64, _P]
+_lib.zero_probe_adam_mix.argtypes = [_P, _P, _P, _P, _P, _i64, _P]
 _lib.zero_shard_step_noalloc.argtypes = _lib.zero_shard_step.argtypes
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
@@ -101,7 +102,8 @@ EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_lamb_plan_create", "zero_lamb_plan_destroy", "zero_lamb_step", "zero_lamb_moments",
            "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async", "zero_shard_apply_async",
            "zero_resident_state_init", "zero_shard_step_resident", "zero_resident_release",
-           "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass", "zero_shard_step_noalloc")
+           "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass", "zero_shard_step_noalloc",
+           "zero_probe_adam_mix")
 for _f in EXPORTS:
     if _f != "zero_last_error":
         getattr(_lib, _f).restype = ctypes.c_int
@@ -429,6 +431,18 @@ def zero_probe_copy(src, dst, nbytes=None, stream=None):
         if not isinstance(t, int) and t.numel() * t.element_size() < nbytes:
             raise ValueError("nbytes = %d exceeds a buffer of %d bytes" % (nbytes, t.numel() * t.element_size()))
     _check(_lib.zero_probe_copy(_addr(src), _addr(dst), int(nbytes), _stream(stream)))
+
+
+def zero_probe_adam_mix(grad16, master32, m32, v32, param16_out, n=None, stream=None):
+    """Enqueue the byte-mix probe of the Adam update over the arrays (it overwrites master32,
+    m32, v32 and param16_out)."""
+    import torch
+    h16 = (torch.float16, torch.int16)
+    f32 = (torch.float32,)
+    n = _shard_len(n, grad16, master32, m32, v32, param16_out)
+    _check(_lib.zero_probe_adam_mix(_addr(grad16, h16, "grad16"), _addr(master32, f32, "master32"),
+                                    _addr(m32, f32, "m32"), _addr(v32, f32, "v32"),
+                                    _addr(param16_out, h16, "param16_out"), int(n), _stream(stream)))
 
 
 def zero_probe_lamb_pass(pass_, grad16, master32, m32, v32, param16_out, n=None, stream=None):

@@ -13,8 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = [os.path.join(CSRC, "zero_shard.hip"), os.path.join(CSRC, "zero_lamb.hip")]
-DEPS = SOURCES + [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "lamb_kernels.hpp", "host_common.hpp")] + [
-    os.path.join(ROOT, "include", "zero_shard.h")]
+DEPS = SOURCES + [os.path.join(CSRC, f) for f in ("shard_kernels.hpp", "lamb_kernels.hpp", "probe_kernels.hpp",
+                                                  "host_common.hpp")] + [os.path.join(ROOT, "include", "zero_shard.h")]
 LIB = os.path.join(PKG, "libzeroshard.so")
 ARCH = "gfx950"
 

@@ -36,11 +36,11 @@ constexpr int64_t kMaxNumel = (int64_t)1 << 40;
 
 // Per-device launch facts, computed once per device (no allocation): compute
 // units and the dynamic-LDS reservations that cap resident workgroups of the
-// streaming kernels (occupancy_lds).
+// streaming kernels (occupancy_lds), the update's byte-mix probe included.
 struct DevInfo {
     int ncu = 0;
-    size_t stats_lds = 0, adam_lds = 0;
-    int stats_resident = 0, adam_resident = 0;
+    size_t stats_lds = 0, adam_lds = 0, probe_adam_lds = 0;
+    int stats_resident = 0, adam_resident = 0, probe_adam_resident = 0;
     int64_t small_cap[4] = {};  // co-resident workgroups of k_small_step<1, 2, 4, 8>
     int64_t small_share = 4;    // a one-launch grid takes at most small_cap / small_share
 };

@@ -26,6 +26,7 @@
 
 #include "zero_shard.h"
 #include "shard_kernels.hpp"
+#include "probe_kernels.hpp"
 #include "host_common.hpp"
 
 namespace zsh {
@@ -226,6 +227,9 @@ int dev_info(int dev, const DevInfo** out) {
                 reinterpret_cast<const void*>(
                     zs::k_adam_vec<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD, kAdamREV, false>),
                 kAdamBlock, kAdamPerCU, prop, &d.adam_resident);
+            d.probe_adam_lds = occupancy_lds(
+                reinterpret_cast<const void*>(zs::k_probe_adam<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD>),
+                kAdamBlock, kAdamPerCU, prop, &d.probe_adam_resident);
             for (int k = 0; k < 4; ++k) {
                 int per_cu = 0;
                 if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, small_kernel(kSmallV[k]), zs::kSmallBlock,
@@ -1416,6 +1420,36 @@ int zero_shard_step_noalloc(const uint16_t* grad16, float* master32, float* m32,
     }
     set_stats(r, n, pl.small_v ? 1 : 0);
     return r.skip ? ZERO_SKIPPED : ZERO_OK;
+}
+
+int zero_probe_adam_mix(const uint16_t* grad16, float* master32, float* m32, float* v32, uint16_t* param16_out,
+                        int64_t n, void* stream_) {
+    const char* fn = "zero_probe_adam_mix";
+    int rc = check_arrays(fn, grad16, master32, m32, v32, param16_out, n);
+    if (rc || n == 0)
+        return rc;
+    const uintptr_t a16[3] = {reinterpret_cast<uintptr_t>(master32), reinterpret_cast<uintptr_t>(m32),
+                              reinterpret_cast<uintptr_t>(v32)};
+    for (int i = 0; i < 3; ++i)
+        if (a16[i] % 16)
+            return fail(ZERO_EINVAL, "%s: fp32 array %d must be 16-byte aligned", fn, i + 1);
+    if (reinterpret_cast<uintptr_t>(grad16) % 8 || reinterpret_cast<uintptr_t>(param16_out) % 8)
+        return fail(ZERO_EINVAL, "%s: grad16 and param16_out must be 8-byte aligned", fn);
+    if ((rc = check_shard_ranges(fn, grad16, master32, m32, v32, param16_out, n)))
+        return rc;
+    hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+    int dev = 0;
+    const DevInfo* info = nullptr;
+    if ((rc = current_device(stream, &dev)) || (rc = dev_info(dev, &info)))
+        return rc;
+    const int64_t nvec = n / 4;
+    int64_t blocks = ceil_div(nvec, (int64_t)kAdamBlock * kAdamUnroll);
+    blocks = blocks < 1 ? 1 : (blocks > kAdamMaxBlocks ? kAdamMaxBlocks : blocks);
+    zs::k_probe_adam<kAdamBlock, kAdamUnroll, kAdamNTL, kAdamNTS, kAdamXCD>
+        <<<(unsigned)blocks, kAdamBlock, info->probe_adam_lds, stream>>>(grad16, master32, m32, v32, param16_out,
+                                                                          n, nvec);
+    HIP_TRY(hipGetLastError());
+    return ZERO_OK;
 }
 
 int zero_probe_copy(const void* src, void* dst, int64_t bytes, void* stream_) {

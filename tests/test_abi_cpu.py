@@ -197,6 +197,21 @@ def test_probe_copy_rejects_without_launching(zb):
     assert "GPU-accessible" in zb.zero_last_error()
 
 
+def test_probe_adam_mix_rejects_without_launching(zb):
+    lib = zb.raw_library()
+    assert lib.zero_probe_adam_mix(*GOOD, -1, None) == zb.ZERO_EINVAL
+    assert lib.zero_probe_adam_mix(0, *GOOD[1:], 10, None) == zb.ZERO_EINVAL                     # NULL
+    assert lib.zero_probe_adam_mix(GOOD[0], GOOD[1] + 4, *GOOD[2:], 10, None) == zb.ZERO_EINVAL  # fp32 not 16-B
+    assert "16-byte" in zb.zero_last_error()
+    assert lib.zero_probe_adam_mix(GOOD[0] + 2, *GOOD[1:], 10, None) == zb.ZERO_EINVAL           # fp16 not 8-B
+    assert "8-byte" in zb.zero_last_error()
+    assert lib.zero_probe_adam_mix(GOOD[0], GOOD[1], GOOD[1] + 16, *GOOD[3:], 10, None) == zb.ZERO_EINVAL  # overlap
+    assert lib.zero_probe_adam_mix(0, 0, 0, 0, 0, 0, None) == zb.ZERO_OK
+    # addresses outside any GPU allocation are refused before a launch
+    assert lib.zero_probe_adam_mix(*GOOD, 64, None) == zb.ZERO_EINVAL
+    assert "GPU-accessible" in zb.zero_last_error()
+
+
 def test_lamb_plan_rejects_bad_tables_without_a_gpu(zb):
     lib = zb.raw_library()
     out = ctypes.c_void_p()

@@ -39,6 +39,15 @@ def test_traffic_summary_matches_the_kernel_sources_or_is_ignored(tmp_path, monk
     assert bench.measured_traffic(workload, n) == 7e9
 
 
+def test_committed_traffic_summaries_match_the_current_kernels():
+    # the counter summaries under profiles/ were taken on the kernel sources as they stand, so the
+    # bench line carries measured traffic for every large workload (a kernel change needs new counters)
+    for workload, n in (("gpt2_1p5b", 93_750_000), ("dp_13b", 203_125_000), ("mp16_dp25_100b", 250_000_000),
+                        ("ragged_1t", 61_034_389)):
+        assert bench.measured_traffic(workload, n) is not None, workload
+    assert bench.measured_lamb_traffic(250_000_000) is not None
+
+
 def test_lamb_traffic_summary_matches_the_kernel_sources_or_is_ignored(tmp_path, monkeypatch):
     t = bench.measured_lamb_traffic(250_000_000)
     if t is not None:  # present and current: within 1 % of the moments pass's 22 B/element

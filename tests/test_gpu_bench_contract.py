@@ -48,6 +48,7 @@ def _check(d, kernel):
 def test_adam_line():
     d = _run()
     _check(d, "k_small_step")
+    assert "adam_probe" not in d  # the one-launch step has no separate update kernel to compare
     cp = d["cpu_baseline_parallel"]
     assert cp["kind"] == "oracle" and cp["cores"] >= 1 and cp["value"] > 0 and cp["unit"] == "params/s"
 
@@ -66,3 +67,6 @@ def test_other_step_forms_print_their_line(mode):
     d = _run(*mode)
     _check(d, "k_adam_vec")
     assert "path" in d["config"]
+    ap = d["adam_probe"]  # the update's byte-mix probe on the same arrays
+    assert ap["kernel"] == "k_probe_adam" and ap["probe_ms"] > 0 and ap["probe_gbps"] > 0
+    assert abs(ap["update_frac_of_probe"] - ap["update_gbps"] / ap["probe_gbps"]) < 1e-12

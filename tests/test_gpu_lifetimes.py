@@ -251,3 +251,23 @@ def test_lamb_probes_touch_exactly_their_arrays(env):
     assert np.array_equal(bufs[1].download(), o)
     assert np.array_equal(bufs[4].download(), o.astype(np.float16).view(np.uint16))
     assert all(b.guards_intact() for b in bufs)
+
+
+def test_adam_probe_touches_exactly_its_arrays(env):
+    # the update's byte-mix probe: reads the gradient and the three fp32 arrays, writes the
+    # fp32 arrays and the fp16 parameters (vectors, then a 3-element tail), nothing beyond them
+    torch, zb, dev = env
+    n = 100_003
+    g16, theta, m, v = workloads.random_case(5500, n)
+    bufs = _alloc(torch, dev, n)
+    for b, a in zip(bufs, (g16, theta, m, v, workloads.p16_sentinel(n))):
+        b.upload(a)
+    zb.zero_probe_adam_mix(*(b.view for b in bufs))
+    torch.cuda.synchronize()
+    gf = g16.view(np.float16).astype(np.float32)
+    th = theta + gf
+    assert np.array_equal(bufs[0].download(), g16)
+    assert np.array_equal(bufs[1].download(), th)
+    assert np.array_equal(bufs[2].download(), m + theta) and np.array_equal(bufs[3].download(), v + m)
+    assert np.array_equal(bufs[4].download(), th.astype(np.float16).view(np.uint16))
+    assert all(b.guards_intact() for b in bufs)
