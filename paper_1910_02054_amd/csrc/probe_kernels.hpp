@@ -14,6 +14,19 @@ namespace zs {
 // in place of Adam.  Its time is the achievable time of the update's streams
 // at the update's launch shape.  Arrays start 16-byte aligned (fp16 8-byte):
 // nvec 4-element vectors, then the last 0..3 elements one by one.
+template <bool NTS>
+__device__ __forceinline__ void probe_vec4(u32x2 gq, f32x4 tq, f32x4 mq, f32x4 vq, f32x4* __restrict__ tv,
+                                           f32x4* __restrict__ mv, f32x4* __restrict__ vv, u32x2* __restrict__ pv,
+                                           int64_t i) {
+    const f32x4 gf = {f16_to_f32(gq.x & 0xFFFFu), f16_to_f32(gq.x >> 16), f16_to_f32(gq.y & 0xFFFFu),
+                      f16_to_f32(gq.y >> 16)};
+    const f32x4 to = tq + gf;
+    st<NTS>(to, tv + i);
+    st<NTS>(mq + tq, mv + i);
+    st<NTS>(vq + mq, vv + i);
+    st<NTS>(u32x2{f32_to_f16(to.x) | (f32_to_f16(to.y) << 16), f32_to_f16(to.z) | (f32_to_f16(to.w) << 16)}, pv + i);
+}
+
 template <int BLOCK, int U, bool NTL, bool NTS, bool XCD>
 __global__ __launch_bounds__(BLOCK) void k_probe_adam(const uint16_t* __restrict__ g, float* __restrict__ th,
                                                       float* __restrict__ m, float* __restrict__ v,
@@ -37,30 +50,29 @@ __global__ __launch_bounds__(BLOCK) void k_probe_adam(const uint16_t* __restrict
     const int64_t ntiles = (nvec + tile - 1) / tile;
     for (int64_t tb = logical_block<XCD>(); tb < ntiles; tb += gridDim.x) {
         const int64_t base = tb * tile + threadIdx.x;
-        u32x2 gq[U];
-        f32x4 tq[U], mq[U], vq[U];
+        // as the update: with one vector per thread, one bounds test around loads, work and stores
+        if constexpr (U == 1) {
+            if (base < nvec)
+                probe_vec4<NTS>(ld<NTL>(gv + base), ld<NTL>(tv + base), ld<NTL>(mv + base), ld<NTL>(vv + base), tv, mv, vv,
+                           pv, base);
+        } else {
+            u32x2 gq[U];
+            f32x4 tq[U], mq[U], vq[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t i = base + (int64_t)u * BLOCK;
-            if (i < nvec) {
-                gq[u] = ld<NTL>(gv + i);
-                tq[u] = ld<NTL>(tv + i);
-                mq[u] = ld<NTL>(mv + i);
-                vq[u] = ld<NTL>(vv + i);
+            for (int u = 0; u < U; ++u) {
+                const int64_t i = base + (int64_t)u * BLOCK;
+                if (i < nvec) {
+                    gq[u] = ld<NTL>(gv + i);
+                    tq[u] = ld<NTL>(tv + i);
+                    mq[u] = ld<NTL>(mv + i);
+                    vq[u] = ld<NTL>(vv + i);
+                }
             }
-        }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int64_t i = base + (int64_t)u * BLOCK;
-            if (i < nvec) {
-                const f32x4 gf = {f16_to_f32(gq[u].x & 0xFFFFu), f16_to_f32(gq[u].x >> 16),
-                                  f16_to_f32(gq[u].y & 0xFFFFu), f16_to_f32(gq[u].y >> 16)};
-                const f32x4 to = tq[u] + gf;
-                st<NTS>(to, tv + i);
-                st<NTS>(mq[u] + tq[u], mv + i);
-                st<NTS>(vq[u] + mq[u], vv + i);
-                st<NTS>(u32x2{f32_to_f16(to.x) | (f32_to_f16(to.y) << 16), f32_to_f16(to.z) | (f32_to_f16(to.w) << 16)},
-                        pv + i);
+            for (int u = 0; u < U; ++u) {
+                const int64_t i = base + (int64_t)u * BLOCK;
+                if (i < nvec)
+                    probe_vec4<NTS>(gq[u], tq[u], mq[u], vq[u], tv, mv, vv, pv, i);
             }
         }
     }
