@@ -7,13 +7,7 @@
 
 namespace zs {
 
-// Byte-mix probe of the update: k_adam_vec's four reads and four writes per
-// element (fp16 gradient, fp32 master, momentum and variance in; fp32 master,
-// momentum, variance and fp16 parameters out), its tiles, vector widths,
-// cache policy and launch shape, with three adds and a conversion per element
-// in place of Adam.  Its time is the achievable time of the update's streams
-// at the update's launch shape.  Arrays start 16-byte aligned (fp16 8-byte):
-// nvec 4-element vectors, then the last 0..3 elements one by one.
+// The probe's work on four consecutive elements: three adds and a conversion.
 template <bool NTS>
 __device__ __forceinline__ void probe_vec4(u32x2 gq, f32x4 tq, f32x4 mq, f32x4 vq, f32x4* __restrict__ tv,
                                            f32x4* __restrict__ mv, f32x4* __restrict__ vv, u32x2* __restrict__ pv,
@@ -27,6 +21,13 @@ __device__ __forceinline__ void probe_vec4(u32x2 gq, f32x4 tq, f32x4 mq, f32x4 v
     st<NTS>(u32x2{f32_to_f16(to.x) | (f32_to_f16(to.y) << 16), f32_to_f16(to.z) | (f32_to_f16(to.w) << 16)}, pv + i);
 }
 
+// Byte-mix probe of the update: k_adam_vec's four reads and four writes per
+// element (fp16 gradient, fp32 master, momentum and variance in; fp32 master,
+// momentum, variance and fp16 parameters out), its tiles, vector widths,
+// cache policy and launch shape, with three adds and a conversion per element
+// in place of Adam.  Its time is the achievable time of the update's streams
+// at the update's launch shape.  Arrays start 16-byte aligned (fp16 8-byte):
+// nvec 4-element vectors, then the last 0..3 elements one by one.
 template <int BLOCK, int U, bool NTL, bool NTS, bool XCD>
 __global__ __launch_bounds__(BLOCK) void k_probe_adam(const uint16_t* __restrict__ g, float* __restrict__ th,
                                                       float* __restrict__ m, float* __restrict__ v,
@@ -53,8 +54,8 @@ __global__ __launch_bounds__(BLOCK) void k_probe_adam(const uint16_t* __restrict
         // as the update: with one vector per thread, one bounds test around loads, work and stores
         if constexpr (U == 1) {
             if (base < nvec)
-                probe_vec4<NTS>(ld<NTL>(gv + base), ld<NTL>(tv + base), ld<NTL>(mv + base), ld<NTL>(vv + base), tv, mv, vv,
-                           pv, base);
+                probe_vec4<NTS>(ld<NTL>(gv + base), ld<NTL>(tv + base), ld<NTL>(mv + base), ld<NTL>(vv + base), tv,
+                                mv, vv, pv, base);
         } else {
             u32x2 gq[U];
             f32x4 tq[U], mq[U], vq[U];
