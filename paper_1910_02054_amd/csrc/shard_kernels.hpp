@@ -490,7 +490,7 @@ __device__ __forceinline__ void adam_vec4(u32x2 gq, f32x4 tq, f32x4 mq, f32x4 vq
 // consecutive vectors.  A tile is BLOCK*U vectors; each thread loads its U
 // vectors of all four inputs before computing (with U = 1, the production
 // shape, the loads, the update and the stores sit under one bounds test,
-// which measured about 5 us faster per 250M-element launch than a separate
+// which measured about 4 us faster per 250M-element launch than a separate
 // test for the loads and for the rest).  Elements [head + 4*nvec, n) are the
 // tail (0..3).  Any grid size is valid (tiles are strided by it).  The fp32
 // constants come by value, or with CDEV from device memory (the resident step
