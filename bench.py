@@ -313,11 +313,17 @@ def main():
         torch.cuda.synchronize()
 
     # the fused step through the binding's prepared call (arrays and stream resolved once; the
-    # library still checks every array on every call)
+    # library still checks every array on every call), driven by the library's loss scaler
     prepared = zb.ShardStepCall(d_gs, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps, w.weight_decay,
                                 w.clip, stream=stream)
 
+    scaled_call = not (args.resident or args.split_phase or lamb)
+
     def step():
+        if scaled_call:
+            # one library call per step: the step at the scaler's t and loss scale on gradient
+            # buffer t mod 2, then the scaler's update (zero_shard_step_scaled)
+            return prepared.scaled(scaler, (scaler.state.applied + 1) & 1)
         d_g = d_gs[scaler.t_next % 2]
         if args.resident == "graph":
             graphs[scaler.t_next % 2].replay()
@@ -345,9 +351,6 @@ def main():
         elif lamb:
             flag = zb.zero_lamb_step(plan, d_g, d_theta, d_m, d_v, d_p, w.lr, w.beta1, w.beta2, w.eps,
                                      w.weight_decay, scaler.t_next, scaler.scale, w.clip, stream=stream)
-        else:
-            t = scaler.t_next
-            flag = prepared(t, scaler.scale, t % 2)
         scaler.update(flag)
         return flag
 

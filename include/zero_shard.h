@@ -334,6 +334,29 @@ typedef struct {
 int zero_scaler_init(zero_scaler_t* s, double scale, int64_t window, double min_scale);
 int zero_scaler_update(zero_scaler_t* s, int32_t skipped);
 
+/* The arguments of zero_shard_step that stay fixed over a training loop: the
+ * shard's five arrays (DEVICE pointers with zero_shard_step's rules), n, the
+ * hyperparameters and the stream (NULL: the default stream). */
+typedef struct {
+    const uint16_t* grad16;
+    float* master32;
+    float* m32;
+    float* v32;
+    uint16_t* param16_out;
+    int64_t n;
+    double lr, beta1, beta2, eps, weight_decay, clip;
+    void* stream;
+} zero_step_args_t;
+
+/* One step of a mixed-precision training loop (Sec. 3.1) in one call: the
+ * shard step of *args at t = scaler->applied + 1 and loss_scale =
+ * scaler->scale, then zero_scaler_update(scaler, skipped).  For loops over
+ * small shards, where the host call is most of the step.  Returns what
+ * zero_shard_step returns (0 applied, 1 skipped); ZERO_EINVAL if args or
+ * scaler is NULL or scaler->applied is negative or INT64_MAX.  On any error
+ * the scaler is left as it was. */
+int zero_shard_step_scaled(const zero_step_args_t* args, zero_scaler_t* scaler);
+
 /* ------------------------------------------------------------------------ */
 /* Model-state memory per device (Sec. 3.1, Sec. 5.1-5.3, Table 1)           */
 /* ------------------------------------------------------------------------ */

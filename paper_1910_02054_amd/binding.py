@@ -41,6 +41,14 @@ class ScalerState(ctypes.Structure):
                 ("applied", ctypes.c_int64), ("good", ctypes.c_int64)]
 
 
+class StepArgs(ctypes.Structure):
+    """Mirror of zero_step_args_t (the fixed arguments of a training loop's step)."""
+    _fields_ = [(k, ctypes.c_void_p) for k in ("grad16", "master32", "m32", "v32", "param16_out")] + \
+               [("n", ctypes.c_int64)] + \
+               [(k, ctypes.c_double) for k in ("lr", "beta1", "beta2", "eps", "weight_decay", "clip")] + \
+               [("stream", ctypes.c_void_p)]
+
+
 class Profile(ctypes.Structure):
     _fields_ = [("steps", ctypes.c_int64), ("stats_ms", ctypes.c_double), ("update_ms", ctypes.c_double)]
 
@@ -76,6 +84,7 @@ _lib.zero_stream_release.argtypes = [_P]
 _lib.zero_workspace_count.argtypes = [ctypes.POINTER(_i64), ctypes.POINTER(_i64)]
 _lib.zero_probe_lamb_pass.argtypes = [_i32, _P, _P, _P, _P, _P, _i64, _P]
 _lib.zero_probe_adam_mix.argtypes = [_P, _P, _P, _P, _P, _i64, _P]
+_lib.zero_shard_step_scaled.argtypes = [_P, _P]
 _lib.zero_shard_step_noalloc.argtypes = _lib.zero_shard_step.argtypes
 _lib.zero_scaler_init.argtypes = [ctypes.POINTER(ScalerState), _dbl, _i64, _dbl]
 _lib.zero_scaler_update.argtypes = [ctypes.POINTER(ScalerState), _i32]
@@ -103,7 +112,7 @@ EXPORTS = ("zero_partition_layout", "zero_shard_step", "zero_shard_stats", "zero
            "zero_lamb_apply", "zero_lamb_profile_read", "zero_shard_stats_async", "zero_shard_apply_async",
            "zero_resident_state_init", "zero_shard_step_resident", "zero_resident_release",
            "zero_stream_release", "zero_workspace_count", "zero_probe_lamb_pass", "zero_shard_step_noalloc",
-           "zero_probe_adam_mix")
+           "zero_probe_adam_mix", "zero_shard_step_scaled")
 for _f in EXPORTS:
     if _f != "zero_last_error":
         getattr(_lib, _f).restype = ctypes.c_int
@@ -220,10 +229,21 @@ class ShardStepCall:
         self._stream = ctypes.c_void_p(_stream(stream))
         self._fn = _lib.zero_shard_step
         self.n = n
+        # zero_step_args_t records, one per gradient buffer, for the scaler-driven call
+        self._args = [StepArgs(g.value, *(a.value for a in self._rest), self._clip.value, self._stream.value)
+                      for g in self._grads]
+        self._args_addr = [ctypes.addressof(a) for a in self._args]
+        self._scaled = _lib.zero_shard_step_scaled
 
     def __call__(self, step, loss_scale, which=0) -> int:
         """One step with t = step on gradient buffer `which`: 0 applied, 1 skipped."""
         rc = self._fn(self._grads[which], *self._rest, step, loss_scale, self._clip, self._stream)
+        return _check(rc) if rc < 0 else rc
+
+    def scaled(self, scaler, which=0) -> int:
+        """One step on gradient buffer `which` at the scaler's t and loss scale, then the
+        scaler's update, in one library call (zero_shard_step_scaled): 0 applied, 1 skipped."""
+        rc = self._scaled(self._args_addr[which], scaler.addr)
         return _check(rc) if rc < 0 else rc
 
 
@@ -384,6 +404,7 @@ class Scaler:
     def __init__(self, scale: float, window: int = 1000, min_scale: float = 1.0):
         self.state = ScalerState()
         _check(_lib.zero_scaler_init(ctypes.byref(self.state), scale, window, min_scale))
+        self.addr = ctypes.addressof(self.state)  # for calls that update the scaler in the library
 
     @property
     def scale(self) -> float:

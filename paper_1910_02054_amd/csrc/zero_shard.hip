@@ -890,6 +890,19 @@ int zero_scaler_update(zero_scaler_t* s, int32_t skipped) {
     return ZERO_OK;
 }
 
+int zero_shard_step_scaled(const zero_step_args_t* a, zero_scaler_t* s) {
+    if (!a || !s)
+        return fail(ZERO_EINVAL, "zero_shard_step_scaled: NULL args or scaler");
+    if (s->applied < 0 || s->applied == INT64_MAX)
+        return fail(ZERO_EINVAL, "zero_shard_step_scaled: scaler has %lld applied steps", (long long)s->applied);
+    const int rc = zero_shard_step(a->grad16, a->master32, a->m32, a->v32, a->param16_out, a->n, a->lr, a->beta1,
+                                   a->beta2, a->eps, a->weight_decay, s->applied + 1, s->scale, a->clip, a->stream);
+    if (rc < 0)
+        return rc;
+    (void)zero_scaler_update(s, rc == ZERO_SKIPPED);
+    return rc;
+}
+
 int zero_shard_last_step_stats(zero_step_stats_t* out) {
     if (!out)
         return fail(ZERO_EINVAL, "zero_shard_last_step_stats: NULL out");

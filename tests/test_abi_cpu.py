@@ -212,6 +212,37 @@ def test_probe_adam_mix_rejects_without_launching(zb):
     assert "GPU-accessible" in zb.zero_last_error()
 
 
+def test_scaled_step_rejects_and_leaves_the_scaler_alone(zb):
+    # the scaler-driven step: argument errors come back before any launch and never touch the
+    # scaler; an empty shard is an applied step (t and the good count advance)
+    lib = zb.raw_library()
+    sc = zb.Scaler(2.0 ** 16, window=3)
+    before = lambda: (sc.state.scale, sc.state.applied, sc.state.good)
+    args = zb.StepArgs(*GOOD, 10, 1e-4, 0.9, 0.999, 1e-8, 0.0, 1.0, None)
+    a = ctypes.addressof(args)
+    assert lib.zero_shard_step_scaled(None, sc.addr) == zb.ZERO_EINVAL
+    assert lib.zero_shard_step_scaled(a, None) == zb.ZERO_EINVAL
+    for field, bad in (("beta1", 1.0), ("lr", float("nan")), ("n", -1), ("grad16", GOOD[0] + 1)):
+        b = zb.StepArgs.from_buffer_copy(args)
+        setattr(b, field, bad)
+        s0 = before()
+        assert lib.zero_shard_step_scaled(ctypes.addressof(b), sc.addr) == zb.ZERO_EINVAL, field
+        assert before() == s0
+    sc.state.applied = -1
+    assert lib.zero_shard_step_scaled(a, sc.addr) == zb.ZERO_EINVAL
+    sc.state.applied = 2 ** 63 - 1
+    assert lib.zero_shard_step_scaled(a, sc.addr) == zb.ZERO_EINVAL
+    assert sc.state.applied == 2 ** 63 - 1
+    sc.state.applied = 0
+    sc.state.scale = 0.0  # an invalid loss scale is the step's own check
+    assert lib.zero_shard_step_scaled(a, sc.addr) == zb.ZERO_EINVAL and sc.state.applied == 0
+    sc.state.scale = 2.0 ** 16
+    empty = zb.StepArgs(0, 0, 0, 0, 0, 0, 1e-4, 0.9, 0.999, 1e-8, 0.0, 1.0, None)
+    for k in range(3):
+        assert lib.zero_shard_step_scaled(ctypes.addressof(empty), sc.addr) == zb.ZERO_OK
+    assert sc.state.applied == 3 and sc.state.good == 0 and sc.state.scale == 2.0 ** 17  # grew at window 3
+
+
 def test_lamb_plan_rejects_bad_tables_without_a_gpu(zb):
     lib = zb.raw_library()
     out = ctypes.c_void_p()
@@ -309,7 +340,7 @@ def test_binding_structs_match_the_c_layout(zb, tmp_path):
         pytest.skip("needs gcc")
     pairs = [("zero_layout_t", zb.Layout), ("zero_step_stats_t", zb.StepStats), ("zero_scaler_t", zb.ScalerState),
              ("zero_profile_t", zb.Profile), ("zero_lamb_profile_t", zb.LambProfile),
-             ("zero_resident_state_t", zb.ResidentState)]
+             ("zero_resident_state_t", zb.ResidentState), ("zero_step_args_t", zb.StepArgs)]
     text = open(HEADER).read()
     lines = ["#include \"zero_shard.h\"", "#include <stdio.h>", "#include <stddef.h>", "int main(void) {"]
     expect = []

@@ -300,3 +300,36 @@ def test_prepared_step_call_equals_the_step(env):
     for x, y in zip(a[1:], b[1:]):
         assert np.array_equal(x.download().view(np.uint8), y.download().view(np.uint8))
     assert all(buf.guards_intact() for buf in a + b)
+
+
+@pytest.mark.parametrize("n", [262_147, 3_000_001])
+def test_scaled_step_follows_the_oracle_and_its_scaler(env, n):
+    # zero_shard_step_scaled: the step at the scaler's t and loss scale, then the scaler's update, in
+    # one call; against the oracle's step and scaler, with an overflow at the third step and the
+    # scale growing after every two good steps (one-launch and three-kernel shards)
+    torch, zb, dev = env
+    _, theta, m, v = workloads.random_case(5700, n)
+    grads = [workloads.random_case(5701 + k, n)[0] for k in range(2)]
+    grads[1][n // 2] = 0x7C00   # the second buffer overflows
+    bufs = _alloc(torch, dev, n)
+    for buf, arr in zip(bufs[1:], (theta, m, v, workloads.p16_sentinel(n))):
+        buf.upload(arr)
+    dg = [torch.from_numpy(g.view(np.int16)).to(dev).view(torch.float16) for g in grads]
+    call = zb.ShardStepCall(dg, *(x.view for x in bufs[1:]), HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], 0.0, 1.0)
+    sc = zb.Scaler(2.0 ** 10, window=2)
+    ref_sc = oracle.Scaler(2.0 ** 10, window=2)
+    ref = [theta.copy(), m.copy(), v.copy(), workloads.p16_sentinel(n)]
+    for k in range(7):
+        which = 1 if k == 2 else 0
+        say("scaled step %d of n=%d (buffer %d)" % (k, n, which))
+        flag = call.scaled(sc, which)
+        skip, _ = H.oracle_step(grads[which], *ref, HP["lr"], HP["beta1"], HP["beta2"], HP["eps"], 0.0,
+                                ref_sc.t_next, ref_sc.scale.value, 1.0)
+        ref_sc.update(skip)
+        assert flag == skip == (1 if which else 0)
+        assert (sc.state.scale, sc.state.applied, sc.state.good) == \
+            (ref_sc.scale.value, ref_sc.applied.value, ref_sc.good.value)
+        assert zb.zero_shard_last_step_stats().path == (1 if n < 1_000_000 else 0)
+    torch.cuda.synchronize()
+    H.compare_state([b.download() for b in bufs[1:]], ref)
+    assert all(b.guards_intact() for b in bufs)
