@@ -40,6 +40,9 @@ typedef struct {
     float lr, b1, omb1, b2, omb2, bc1, bc2, eps, wd;
 } zo_hyper_t;
 void zo_hyper(double lr, double beta1, double beta2, double eps, double wd, int64_t t, zo_hyper_t* h);
+/* The oracle's loss-scale schedule. */
+void zo_scaler_update(double* scale, int64_t* applied, int64_t* good, int32_t skipped, int64_t window,
+                      double min_scale);
 
 #define LR 1e-4
 #define B1 0.9
@@ -199,6 +202,42 @@ static int run_case(int64_t n, const int shift[5], hipStream_t stream) {
             ok = 0;
         } else {
             ok = check_all(&s, n, what);
+        }
+    }
+    if (ok && n > 0) {
+        /* two scaler-driven steps, the second skipped (window 1: the scale doubles after every
+           applied step); the library's scaler against the oracle's schedule */
+        zero_scaler_t sc;
+        if (zero_scaler_init(&sc, SCALE, 1, 1.0) != ZERO_OK) {
+            printf("FAIL: zero_scaler_init\n");
+            ok = 0;
+        }
+        sc.applied = t - 1;
+        double o_scale = SCALE;
+        int64_t o_applied = t - 1, o_good = 0;
+        const zero_step_args_t args = {(const uint16_t*)s.view[0], (float*)s.view[1], (float*)s.view[2],
+                                       (float*)s.view[3], (uint16_t*)s.view[4], n, LR, B1, B2, EPS, WD, CLIP,
+                                       stream};
+        for (int k = 0; k < 2 && ok; ++k) {
+            for (int64_t j = 0; j < n; ++j)
+                s.g[j] = rnd_f16();
+            if (k == 1)
+                s.g[0] = 0x7E00; /* NaN: skipped */
+            upload(&s, 0, s.g, n);
+            const int rc = zero_shard_step_scaled(&args, &sc);
+            HIPCHECK(hipStreamSynchronize(stream));
+            const int want = zo_shard_step(s.g, s.th, s.m, s.v, s.p, n, LR, B1, B2, EPS, WD, o_applied + 1, o_scale,
+                                           CLIP, NULL);
+            zo_scaler_update(&o_scale, &o_applied, &o_good, want, 1, 1.0);
+            snprintf(what, sizeof what, "n=%lld scaled step %d", (long long)n, k);
+            if (rc != want || sc.scale != o_scale || sc.applied != o_applied || sc.good != o_good) {
+                printf("FAIL: %s: returned %d (%s), the oracle %d; scaler (%g, %lld, %lld), oracle (%g, %lld, %lld)\n",
+                       what, rc, zero_last_error(), want, sc.scale, (long long)sc.applied, (long long)sc.good,
+                       o_scale, (long long)o_applied, (long long)o_good);
+                ok = 0;
+            } else {
+                ok = check_all(&s, n, what);
+            }
         }
     }
     for (int i = 0; i < 5; ++i)
