@@ -208,7 +208,8 @@ class ShardStepCall:
     reduce-scatter, or one of a few such buffers): the tensors are checked here as
     zero_shard_step checks them, referenced for the object's lifetime (their storage must not
     be resized or swapped meanwhile), and each call passes only t, the loss scale and which
-    gradient buffer to use.  The library still checks every array's allocation on every call.
+    gradient buffer to use (or, through `scaled`, a Scaler whose t and loss scale the library
+    reads and updates).  The library still checks every array's allocation on every call.
     `stream` is taken now (None: torch's current stream at construction)."""
 
     def __init__(self, grads, master32, m32, v32, param16_out, lr, beta1, beta2, eps, weight_decay, clip,
