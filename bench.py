@@ -240,7 +240,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs one data-parallel rank on one GPU; --gpus %d is not supported "
+        print("bench.py: the benchmark runs one data-parallel rank on one GPU; --gpus %d is not supported "
               "(the shard step needs no collective on one rank)" % max(args.gpus, world), file=sys.stderr)
         sys.exit(2)
 
